@@ -1,0 +1,48 @@
+"""Each plausible mistake, planted in a copy of the oracle source and built
+on the CPU, must make at least one pin fail: the pins have teeth."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+MUTATIONS = {
+    "pad offset dropped": ("ho * p->sh - p->pt + kh", "ho * p->sh + kh"),
+    "left pad used for rows": ("ho * p->sh - p->pt + kh", "ho * p->sh - p->pl + kh"),
+    "filter flipped": ("double fv = (double)p->f[((kh * p->KW + kw)",
+                       "double fv = (double)p->f[(((p->KH - 1 - kh) * p->KW + (p->KW - 1 - kw))"),
+    "filter taps transposed": ("p->f[((kh * p->KW + kw) * p->C + ci)", "p->f[((kw * p->KH + kh) * p->C + ci)"),
+    "input channels reversed": ("p->W + iw) * p->C + ci]", "p->W + iw) * p->C + (p->C - 1 - ci)]"),
+    "stride ignored on columns": ("int64_t iw = wo * p->sw - p->pl + kw;", "int64_t iw = wo - p->pl + kw;"),
+    "no bounds check": ("int inside = ih >= 0 && ih < p->H && iw >= 0 && iw < p->W;",
+                        "int inside = ih >= 0 && iw >= 0 && ih * p->W + iw < p->H * p->W;"),
+    "op(A) transpose reversed": ("return ta ? (double)A[k * lda + i] : (double)A[i * lda + k];",
+                                 "return ta ? (double)A[i * lda + k] : (double)A[k * lda + i];"),
+    "op(B) uses K for ld": ("return tb ? (double)B[j * ldb + k] : (double)B[k * ldb + j];",
+                            "return tb ? (double)B[j * ldb + k] : (double)B[k * (ldb - (ldb > 1)) + j];"),
+    "beta term dropped": ("if (beta != 0.0) r += beta * (double)C[i * ldc + j];", ""),
+    "C always read": ("if (beta != 0.0) r += beta", "r += beta"),
+    "alpha applied twice": ("double r = alpha * s;", "double r = alpha * alpha * s;"),
+    "scale without abs": ("t += fabs(p);", "t += p;"),
+    "conv scale without abs": ("t += fabs(prod);", "t += prod;"),
+    "last k dropped": ("for (int64_t k = 0; k < K; ++k)", "for (int64_t k = 0; k + 1 < K; ++k)"),
+    "last channel dropped": ("for (int64_t ci = 0; ci < p->C; ++ci)", "for (int64_t ci = 0; ci + 1 < p->C; ++ci)"),
+    "output size rounds up": ("*Ho = hspan / sh + 1;", "*Ho = (hspan + sh - 1) / sh + 1;"),
+    "same pads extra on top": ("pads_tlbr[0] = ph / 2;", "pads_tlbr[0] = ph - ph / 2;"),
+    "same size floor": ("int64_t ho = (H + sh - 1) / sh, wo = (W + sw - 1) / sw;",
+                        "int64_t ho = H / sh, wo = W / sw;"),
+}
+
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_is_caught(name, tmp_path):
+    oracle.build(force=False)
+    proc = subprocess.run([sys.executable, "-m", "tests.mutant_runner", name, str(tmp_path)],
+                          cwd=ROOT, capture_output=True, text=True, timeout=300)
+    out = proc.stdout.strip().splitlines()
+    assert out and out[-1].startswith("CAUGHT"), (name, proc.returncode, proc.stdout[-2000:], proc.stderr[-2000:])
