@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Throughput of the parameterized fp32 GEMM / convolution path on one MI355X.
+
+One step runs, once each and back to back on one stream:
+  - the three 4096^3 GEMMs C = A op(B) + 0.5 C in the NN, TN and NT layouts;
+  - the first conv layer of each VGG-16 block at batch 32 (3x3, stride 1,
+    "same" padding): 224x224x3->64, 112x112x64->128, 56x56x128->256,
+    28x28x256->512, 14x14x512->512;
+  - five ResNet-50 bottleneck convolutions at batch 32: 56x56x64 1x1->64,
+    3x3->64, 1x1->256; 56x56x256 1x1 stride 2->128; 7x7x2048 1x1->512.
+All inputs are seeded synthetic fp32 values, uniform on [-1, 1), resident in
+device memory before timing starts.  value = nominal flops of one step
+(2*M*N*K per GEMM, 2*N*Ho*Wo*Cout*KH*KW*Cin per convolution) / time per step.
+
+The JSON line also carries, for the kernel launch with the largest share of
+the step, its fraction of the fp32 matrix peak (HIP events around each of its
+launches on the launch stream), per-op figures, and the CPU oracle's rate on a
+bounded sample of the same work.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fp32 GFLOP/s & % of MI355X fp32 MFMA peak: GEMM 4096³, VGG/ResNet conv layers"
+FP32_MFMA_PEAK_TFLOPS = 157.3   # 256 CUs x 256 flop/clk x 2.4 GHz
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target wall time of the CPU oracle sample (0 skips it)")
+    return ap.parse_args()
+
+
+class Op:
+    def __init__(self, name, flops, bytes_, run, kind):
+        self.name = name
+        self.flops = flops
+        self.bytes = bytes_
+        self.run = run
+        self.kind = kind
+        self.config = ""
+
+
+def make_ops(torch, pk, wl):
+    ops = []
+    host = {}
+    for case in wl.STEP_GEMMS:
+        A, B, C = case.inputs()
+        host[case.name] = ("gemm", case, (A, B, C))
+        dA, dB, dC = (torch.from_numpy(v).cuda() for v in (A, B, C))
+        ta, tb = case.trans_a == "T", case.trans_b == "T"
+
+        def run(dA=dA, dB=dB, dC=dC, case=case, ta=ta, tb=tb):
+            pk.gemm(dA, dB, dC, alpha=case.alpha, beta=case.beta, trans_a=ta, trans_b=tb)
+
+        nbytes = 4 * (case.M * case.K + case.K * case.N + 2 * case.M * case.N)
+        ops.append(Op(case.name, case.flops, nbytes, run, "gemm"))
+    for case in wl.STEP_CONVS:
+        x, f = case.inputs()
+        host[case.name] = ("conv", case, (x, f))
+        N, H, W, Cin = case.x_shape
+        KH, KW, _, Cout = case.f_shape
+        Ho, Wo = pk.conv2d_out_dims(H, W, KH, KW, *case.stride, *case.pads)
+        dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+        dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+        wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
+        ws = torch.empty(wsb // 4, dtype=torch.float32, device="cuda") if wsb else None
+
+        def run(dx=dx, df=df, dy=dy, ws=ws, case=case):
+            pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads, out=dy, workspace=ws)
+
+        sh, sw = case.stride
+        # input bytes the layer must read: every pixel for stride 1, the sampled ones otherwise
+        in_px = N * (H if sh == 1 else Ho) * (W if sw == 1 else Wo) if KH == 1 and KW == 1 else N * H * W
+        nbytes = 4 * (in_px * Cin + KH * KW * Cin * Cout + N * Ho * Wo * Cout)
+        ops.append(Op(case.name, wl.conv_flops(case, Ho, Wo), nbytes, run, "conv"))
+    return ops, host
+
+
+def cpu_baseline(oracle, host, ops, seconds, np):
+    """The oracle on the same fraction of every op's outputs, scaled to GFLOP/s."""
+    rng = np.random.default_rng(2024)
+
+    def run_fraction(frac):
+        flops = 0
+        n_out = 0
+        t0 = time.perf_counter()
+        for op in ops:
+            kind, case, arrs = host[op.name]
+            if kind == "gemm":
+                A, B, C = arrs
+                total = case.M * case.N
+                n = max(1, int(round(total * frac)))
+                flat = rng.integers(0, total, n)
+                rows, cols = flat // case.N, flat % case.N
+                oracle.sgemm_at(case.trans_a, case.trans_b, case.M, case.N, case.K, case.alpha,
+                                A, case.lda, B, case.ldb, case.beta, C, case.ldc, rows, cols)
+                flops += 2 * case.K * n
+            else:
+                x, f = arrs
+                total = op.flops // (2 * case.KH * case.KW * case.Cin)
+                n = max(1, int(round(total * frac)))
+                flat = rng.integers(0, total, n)
+                oracle.conv2d_at(x, f, case.stride, case.pads, flat)
+                flops += 2 * case.KH * case.KW * case.Cin * n
+            n_out += n
+        return flops, n_out, time.perf_counter() - t0
+
+    step_flops = sum(op.flops for op in ops)
+    frac = 2e8 / step_flops  # calibration: about 0.2 GFLOP
+    f0, _, t0 = run_fraction(frac)
+    frac = min(frac * seconds / max(t0, 1e-3), 1.0)
+    flops, n_out, t = run_fraction(frac)
+    return {
+        "value": round(flops / t / 1e9, 3),
+        "unit": "GFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": "%d outputs drawn uniformly from every op of one step (fraction %.3g of each op's "
+                  "outputs, %.2f GFLOP nominal, fp64 accumulation), %.1f s" % (n_out, frac, flops / 1e9, t),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (requested --gpus %d)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_1904_05347_amd as pk
+    from paper_1904_05347_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    pk.load()
+    print("bench: generating inputs", file=sys.stderr, flush=True)
+    ops, host = make_ops(torch, pk, wl)
+    stream = torch.cuda.current_stream()
+
+    # one untimed pass records which configuration each op runs
+    for op in ops:
+        op.run()
+        op.config = pk.last_config_name()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        for op in ops:
+            op.run()
+    torch.cuda.synchronize()
+    print("bench: warmed up, timing %d steps" % args.steps, file=sys.stderr, flush=True)
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for s in range(args.steps):
+        for i, op in enumerate(ops):
+            ev[s][i].record(stream)
+            op.run()
+        ev[s][len(ops)].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / args.steps
+    step_flops = sum(op.flops for op in ops)
+    value = step_flops / (ms_per_step * 1e-3) / 1e9
+
+    per_op = []
+    for i, op in enumerate(ops):
+        ms = sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(args.steps)) / args.steps
+        tflops = op.flops / (ms * 1e-3) / 1e12
+        per_op.append({"op": op.name, "config": op.config, "ms": round(ms, 4),
+                       "tflops": round(tflops, 2), "frac_mfma_peak": round(tflops / FP32_MFMA_PEAK_TFLOPS, 4),
+                       "gbs": round(op.bytes / (ms * 1e-3) / 1e9, 1)})
+    dom = max(range(len(ops)), key=lambda i: per_op[i]["ms"])
+    d = per_op[dom]
+    roofline = {"bound": "mfma", "achieved": d["tflops"], "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(d["tflops"] / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                "kernel": d["config"], "workload": d["op"], "avg_launch_ms": d["ms"],
+                "flops_per_launch": ops[dom].flops}
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+        print("bench: timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(oracle, host, ops, args.cpu_seconds, np)
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "gemm 4096^3 NN/TN/NT beta=0.5 + vgg16 conv{1..5}_1 b32 + "
+                               "resnet50 bottleneck convs b32 (13 ops per step)",
+                   "frac_mfma_peak": round(value / 1e3 / FP32_MFMA_PEAK_TFLOPS, 4),
+                   "step_gflop": round(step_flops / 1e9, 3)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "per_op": per_op,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,180 @@
+/*
+ * pk.h -- parameterized fp32 GEMM and 2-D convolution forward for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The operations are those of "Cross-Platform Performance Portability Using
+ * Highly Parametrized SYCL Kernels" (Lawson et al., arXiv 1904.05347):
+ *   - GEMM, Section 3.1: C = alpha * op(A) * op(B) + beta * C, with op the
+ *     identity or the transpose;
+ *   - convolution forward, Section 4.1 (Algorithm 1 and the centred-window
+ *     formula after it): an NHWC input, an HWIO filter (the paper's
+ *     H x W x C input, R x S x C x K filter), cross-correlation (no filter
+ *     flip), with the stride and window of the paper's layer tables and
+ *     explicit zero padding.
+ *
+ * Conventions shared by every call:
+ *   - Every tensor pointer is a DEVICE pointer to fp32 data.  The caller owns
+ *     all memory; the library allocates no device memory and keeps no pointer
+ *     after a call returns.
+ *   - Storage is row-major (C order).  A column-major caller maps onto the
+ *     same call by swapping the operands: the column-major product
+ *     C = alpha op(A) op(B) + beta C is pk_sgemm(transB, transA, N, M, K,
+ *     alpha, B, ldb, A, lda, beta, C, ldc).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ *     asynchronous and ordered on that stream; results are valid once it
+ *     has synchronised.  No call synchronises the device.
+ *   - Outputs must not overlap inputs.
+ *   - Every call returns a pk_status.  Invalid arguments are detected before
+ *     any work is queued; pk_last_invalid_param() then names the 1-based
+ *     position of the offending argument.  Nothing aborts and no C++
+ *     exception crosses this interface.
+ *   - Thread safety: calls may come from several host threads at once.  The
+ *     "last" queries below report the calling thread's most recent call.
+ */
+#ifndef PK_H
+#define PK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PK_OK = 0,
+    PK_ERR_INVALID_VALUE = 1, /* an argument is out of range; see pk_last_invalid_param() */
+    PK_ERR_NOT_SUPPORTED = 2, /* a well-formed request this library does not implement */
+    PK_ERR_WORKSPACE = 3,     /* a forced split-K configuration lacks workspace */
+    PK_ERR_LAUNCH = 4         /* the HIP runtime refused a kernel launch */
+} pk_status;
+
+/*
+ * Single-precision GEMM (Section 3.1):  C <- alpha * op(A) * op(B) + beta * C.
+ *
+ *   transA, transB  'N'/'n' (op = identity) or 'T'/'t'/'C'/'c' (op = transpose;
+ *                   'C' equals 'T' for real data).
+ *   M, N, K         op(A) is M x K, op(B) is K x N, C is M x N.  Each >= 0.
+ *   A, lda          row-major; M x K with lda >= max(1, K) for 'N',
+ *                   K x M with lda >= max(1, M) for 'T'.
+ *   B, ldb          row-major; K x N with ldb >= max(1, N) for 'N',
+ *                   N x K with ldb >= max(1, K) for 'T'.
+ *   C, ldc          row-major M x N, ldc >= max(1, N).  Read only if beta != 0.
+ *
+ * Quick returns (netlib BLAS semantics): M == 0 or N == 0 does nothing;
+ * alpha == 0 or K == 0 sets C <- beta * C without reading A or B;
+ * beta == 0 writes C without reading it, so NaN or Inf in C is not propagated.
+ * A and B may be NULL only when they are not read.
+ * Results are deterministic: the same call on the same device gives the same
+ * bits (no atomics; any split of K is reduced in a fixed order).
+ */
+int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K,
+             float alpha, const float *A, int64_t lda,
+             const float *B, int64_t ldb,
+             float beta, float *C, int64_t ldc, void *stream);
+
+/*
+ * Output size of a convolution window (the stride S and window W columns of
+ * the paper's layer tables): Ho = floor((H + pt + pb - KH) / sh) + 1, and the
+ * same for Wo.  Pads >= 0, strides >= 1, window >= 1 and not larger than the
+ * padded image.  Host-only; touches no GPU.
+ */
+int pk_conv2d_out_dims(int64_t H, int64_t W, int64_t KH, int64_t KW,
+                       int64_t sh, int64_t sw, int64_t pt, int64_t pl,
+                       int64_t pb, int64_t pr, int64_t *Ho, int64_t *Wo);
+
+/*
+ * "SAME" padding: the output keeps ceil(H / sh) x ceil(W / sw) pixels and the
+ * least total padding that gives it is split with the odd pixel at the
+ * bottom/right.  pads_tlbr receives {top, left, bottom, right}.  Host-only.
+ */
+int pk_conv2d_same_pads(int64_t H, int64_t W, int64_t KH, int64_t KW,
+                        int64_t sh, int64_t sw, int64_t pads_tlbr[4]);
+
+/*
+ * Bytes of device workspace that lets pk_conv2d_fwd split the reduction
+ * (KH * KW * Cin) of this problem across work-groups; 0 when the chosen
+ * configuration needs none.  Host-only.
+ */
+size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin,
+                                 int64_t KH, int64_t KW, int64_t Cout,
+                                 int64_t sh, int64_t sw, int64_t pt, int64_t pl,
+                                 int64_t pb, int64_t pr);
+
+/*
+ * 2-D convolution forward (Section 4.1, Algorithm 1 with a centred, zero-
+ * padded window):
+ *   y[n][ho][wo][co] = sum_{kh, kw, ci} x~[n][ho*sh - pt + kh][wo*sw - pl + kw][ci]
+ *                                       * f[kh][kw][ci][co]
+ * where x~ is x inside the H x W image and 0 outside.
+ *
+ *   x            N x H x W x Cin, contiguous (NHWC).
+ *   f            KH x KW x Cin x Cout, contiguous (HWIO).
+ *   sh, sw       strides >= 1.  pt, pl, pb, pr: zero padding >= 0.
+ *   y            N x Ho x Wo x Cout, contiguous (NHWC).  Ho, Wo must equal
+ *                pk_conv2d_out_dims() of the geometry (else INVALID_VALUE).
+ *   workspace    optional device buffer of workspace_bytes; with at least
+ *                pk_conv2d_workspace_bytes() the reduction may be split for
+ *                small outputs.  NULL / too small selects an unsplit
+ *                configuration.  Contents on return are unspecified.
+ * N == 0 does nothing.  Dilation, groups, bias and activation are not part
+ * of this operation.
+ */
+int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                  const float *f, int64_t KH, int64_t KW, int64_t Cout,
+                  int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb, int64_t pr,
+                  float *y, int64_t Ho, int64_t Wo,
+                  void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static text for a status code. */
+const char *pk_status_string(int status);
+
+/* 1-based argument position of this thread's last PK_ERR_INVALID_VALUE, 0 if none. */
+int pk_last_invalid_param(void);
+
+/* Name of the compiled configuration this thread's last successful call ran
+ * ("" for quick returns).  Static storage. */
+const char *pk_last_config_name(void);
+
+/*
+ * The compiled tile-parameter space.  Each configuration is one kernel
+ * instance: work-group tile BM x BN, K-block depth BK, a wave grid, the
+ * operand layouts it reads, its vector load widths and its LDS footprint.
+ */
+typedef struct {
+    const char *name;
+    int kind;        /* 0 = GEMM, 1 = implicit-GEMM convolution */
+    int bm, bn, bk;  /* work-group tile and K-block depth */
+    int waves_m, waves_n; /* wave grid; each wave owns (bm/waves_m) x (bn/waves_n) */
+    int threads;     /* work-group size */
+    int trans_a, trans_b; /* operand layouts read (1 = transposed storage) */
+    int vec_a, vec_b; /* elements per global load */
+    int stages;      /* LDS buffers (2 = double buffered) */
+    int lds_bytes;   /* LDS per work-group */
+} pk_config_info;
+
+int pk_num_configs(void);
+/* Fills *info for configuration idx (0 <= idx < pk_num_configs()). */
+int pk_get_config(int idx, pk_config_info *info);
+
+/*
+ * Forces every later call on this thread to use the named configuration
+ * (NULL or "" restores the selector).  A forced configuration that cannot run
+ * a given call (wrong layout, alignment, kind) makes that call return
+ * PK_ERR_NOT_SUPPORTED.  Unknown names give PK_ERR_INVALID_VALUE.  The
+ * environment variable PK_FORCE_CONFIG, read at first use, sets the same
+ * override for threads that never call this; if it names no configuration,
+ * every pk_sgemm / pk_conv2d_fwd call returns PK_ERR_INVALID_VALUE with
+ * pk_last_invalid_param() == 0.
+ */
+int pk_force_config(const char *name);
+
+/* Forces the split factor of later convolution calls on this thread
+ * (0 restores the selector's choice). */
+int pk_force_splits(int splits);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PK_H */

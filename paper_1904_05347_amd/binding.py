@@ -1,0 +1,260 @@
+"""Python mirror of the C-ABI in include/pk.h (argument marshalling only).
+
+Every call goes through libpk.so; there is no other compute path.  The
+library must have been built (``python -m paper_1904_05347_amd.build``); a
+missing library raises ``PkLibraryMissing`` instead of falling back to
+anything.  torch is imported before the library is loaded so that both share
+the one HIP runtime that torch brings.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpk.so")
+
+PK_OK = 0
+PK_ERR_INVALID_VALUE = 1
+PK_ERR_NOT_SUPPORTED = 2
+PK_ERR_WORKSPACE = 3
+PK_ERR_LAUNCH = 4
+
+_lib = None
+_i64 = ctypes.c_int64
+_p = ctypes.c_void_p
+
+
+class PkLibraryMissing(RuntimeError):
+    pass
+
+
+class PkError(RuntimeError):
+    def __init__(self, status: int, what: str, param: int = 0):
+        self.status = status
+        self.param = param
+        msg = "%s: %s" % (what, _lib.pk_status_string(status).decode() if _lib else status)
+        if status == PK_ERR_INVALID_VALUE:
+            msg += " (argument %d)" % param
+        super().__init__(msg)
+
+
+class ConfigInfo(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char_p), ("kind", ctypes.c_int),
+                ("bm", ctypes.c_int), ("bn", ctypes.c_int), ("bk", ctypes.c_int),
+                ("waves_m", ctypes.c_int), ("waves_n", ctypes.c_int), ("threads", ctypes.c_int),
+                ("trans_a", ctypes.c_int), ("trans_b", ctypes.c_int),
+                ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
+                ("stages", ctypes.c_int), ("lds_bytes", ctypes.c_int)]
+
+
+# Every symbol include/pk.h declares, with its ctypes signature.
+SIGNATURES = {
+    "pk_sgemm": (ctypes.c_int, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64, ctypes.c_float, _p, _i64,
+                                _p, _i64, ctypes.c_float, _p, _i64, _p]),
+    "pk_conv2d_out_dims": (ctypes.c_int, [_i64] * 10 + [_p, _p]),
+    "pk_conv2d_same_pads": (ctypes.c_int, [_i64] * 6 + [_p]),
+    "pk_conv2d_workspace_bytes": (ctypes.c_size_t, [_i64] * 13),
+    "pk_conv2d_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
+                                     _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
+                                     _p, ctypes.c_size_t, _p]),
+    "pk_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "pk_last_invalid_param": (ctypes.c_int, []),
+    "pk_last_config_name": (ctypes.c_char_p, []),
+    "pk_num_configs": (ctypes.c_int, []),
+    "pk_get_config": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ConfigInfo)]),
+    "pk_force_config": (ctypes.c_int, [ctypes.c_char_p]),
+    "pk_force_splits": (ctypes.c_int, [ctypes.c_int]),
+}
+
+
+def load():
+    """Load libpk.so (once).  Raises PkLibraryMissing when it was not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise PkLibraryMissing("libpk.so is not built: run `python -m paper_1904_05347_amd.build`")
+    try:
+        import torch  # noqa: F401  (load torch's HIP runtime first: one runtime per process)
+    except ImportError:
+        pass
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != PK_OK:
+        raise PkError(status, what, _lib.pk_last_invalid_param())
+
+
+def _trans(t) -> bytes:
+    if isinstance(t, bool):
+        return b"T" if t else b"N"
+    return str(t).encode()[:1]
+
+
+# ------------------------------------------------------------- raw entry points
+
+def sgemm(trans_a, trans_b, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream=None) -> int:
+    """pk_sgemm on raw device addresses; returns the status code."""
+    return load().pk_sgemm(_trans(trans_a), _trans(trans_b), M, N, K, alpha, A, lda, B, ldb,
+                           beta, C, ldc, stream)
+
+
+def conv2d_fwd_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo,
+                   workspace=None, workspace_bytes=0, stream=None) -> int:
+    """pk_conv2d_fwd on raw device addresses; returns the status code."""
+    return load().pk_conv2d_fwd(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr,
+                                y, Ho, Wo, workspace, workspace_bytes, stream)
+
+
+def conv2d_out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr):
+    ho, wo = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().pk_conv2d_out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr,
+                                     ctypes.addressof(ho), ctypes.addressof(wo)), "pk_conv2d_out_dims")
+    return ho.value, wo.value
+
+
+def conv2d_same_pads(H, W, KH, KW, sh, sw):
+    pads = (ctypes.c_int64 * 4)()
+    _check(load().pk_conv2d_same_pads(H, W, KH, KW, sh, sw, ctypes.addressof(pads)), "pk_conv2d_same_pads")
+    return tuple(pads)
+
+
+def conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, sh, sw, pt, pl, pb, pr) -> int:
+    return load().pk_conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, sh, sw, pt, pl, pb, pr)
+
+
+def last_config_name() -> str:
+    return load().pk_last_config_name().decode()
+
+
+def last_invalid_param() -> int:
+    return load().pk_last_invalid_param()
+
+
+def configs():
+    lib = load()
+    out = []
+    for i in range(lib.pk_num_configs()):
+        info = ConfigInfo()
+        _check(lib.pk_get_config(i, ctypes.byref(info)), "pk_get_config")
+        d = {k: getattr(info, k) for k, _ in ConfigInfo._fields_}
+        d["name"] = d["name"].decode()
+        out.append(d)
+    return out
+
+
+def force_config(name):
+    _check(load().pk_force_config(name.encode() if name else None), "pk_force_config")
+
+
+def force_splits(n: int):
+    _check(load().pk_force_splits(int(n)), "pk_force_splits")
+
+
+# ------------------------------------------------------------ torch tensors
+
+def _stream_handle(tensor):
+    import torch
+    return torch.cuda.current_stream(tensor.device).cuda_stream
+
+
+def _check_f32_cuda(t, what):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float32 or not t.is_cuda:
+        raise TypeError("%s must be a float32 tensor on a HIP device" % what)
+
+
+def _ld_2d(t, what):
+    """Leading dimension of a row-major 2-D view (unit column stride)."""
+    if t.dim() != 2:
+        raise ValueError("%s must be 2-D" % what)
+    if t.size(1) > 1 and t.stride(1) != 1:
+        raise ValueError("%s must have unit column stride" % what)
+    return max(t.stride(0), t.size(1), 1)
+
+
+def gemm(a, b, c=None, alpha=1.0, beta=0.0, trans_a=False, trans_b=False):
+    """C = alpha * op(a) @ op(b) + beta * c on the current stream.
+
+    ``a`` is stored M x K (or K x M with trans_a), ``b`` K x N (or N x K with
+    trans_b); both are row-major views with unit column stride.  Returns c
+    (allocated when None; then beta must be 0).
+    """
+    import torch
+    _check_f32_cuda(a, "a")
+    _check_f32_cuda(b, "b")
+    lda, ldb = _ld_2d(a, "a"), _ld_2d(b, "b")
+    M, K = (a.size(1), a.size(0)) if trans_a else (a.size(0), a.size(1))
+    Kb, N = (b.size(1), b.size(0)) if trans_b else (b.size(0), b.size(1))
+    if Kb != K:
+        raise ValueError("inner dimensions differ: %d vs %d" % (K, Kb))
+    if c is None:
+        if beta != 0.0:
+            raise ValueError("beta != 0 needs c")
+        c = torch.empty((M, N), dtype=torch.float32, device=a.device)
+    _check_f32_cuda(c, "c")
+    if tuple(c.shape) != (M, N):
+        raise ValueError("c must be %d x %d" % (M, N))
+    ldc = _ld_2d(c, "c")
+    st = sgemm(bool(trans_a), bool(trans_b), M, N, K, float(alpha), a.data_ptr(), lda,
+               b.data_ptr(), ldb, float(beta), c.data_ptr(), ldc, _stream_handle(c))
+    _check(st, "pk_sgemm")
+    return c
+
+
+def resolve_padding(padding, H, W, KH, KW, sh, sw):
+    if isinstance(padding, str):
+        p = padding.upper()
+        if p == "VALID":
+            return (0, 0, 0, 0)
+        if p == "SAME":
+            return conv2d_same_pads(H, W, KH, KW, sh, sw)
+        raise ValueError("padding must be 'SAME', 'VALID' or (top, left, bottom, right)")
+    pads = tuple(int(v) for v in padding)
+    if len(pads) != 4:
+        raise ValueError("padding must be (top, left, bottom, right)")
+    return pads
+
+
+def conv2d_fwd(x, w, stride=(1, 1), padding="SAME", out=None, workspace=None):
+    """NHWC x (N, H, W, Cin) convolved with HWIO w (KH, KW, Cin, Cout).
+
+    ``padding`` is 'SAME', 'VALID' or (top, left, bottom, right).  The
+    workspace (a float32 device tensor) is optional; it lets small outputs
+    split their reduction (see ``conv2d_workspace_bytes``).
+    """
+    import torch
+    _check_f32_cuda(x, "x")
+    _check_f32_cuda(w, "w")
+    if x.dim() != 4 or w.dim() != 4:
+        raise ValueError("x is N x H x W x Cin, w is KH x KW x Cin x Cout")
+    if not x.is_contiguous() or not w.is_contiguous():
+        raise ValueError("x and w must be contiguous (NHWC / HWIO)")
+    N, H, W, Cin = x.shape
+    KH, KW, Cin2, Cout = w.shape
+    if Cin2 != Cin:
+        raise ValueError("input channels differ: %d vs %d" % (Cin, Cin2))
+    sh, sw = (stride, stride) if isinstance(stride, int) else tuple(stride)
+    pt, pl, pb, pr = resolve_padding(padding, H, W, KH, KW, sh, sw)
+    Ho, Wo = conv2d_out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr)
+    if out is None:
+        out = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device=x.device)
+    _check_f32_cuda(out, "out")
+    if tuple(out.shape) != (N, Ho, Wo, Cout) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous %s tensor" % ((N, Ho, Wo, Cout),))
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        _check_f32_cuda(workspace, "workspace")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * 4
+    st = conv2d_fwd_raw(x.data_ptr(), N, H, W, Cin, w.data_ptr(), KH, KW, Cout, sh, sw,
+                        pt, pl, pb, pr, out.data_ptr(), Ho, Wo, ws_ptr, ws_bytes, _stream_handle(out))
+    _check(st, "pk_conv2d_fwd")
+    return out

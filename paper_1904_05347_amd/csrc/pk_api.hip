@@ -1,0 +1,554 @@
+// pk_api.hip -- the C-ABI: argument checks, shape derivation, the per-shape
+// parameter selector and the launches.
+//
+// The selector is the runtime half of the paper's parameterization: the
+// kernels are compiled for a fixed set of tile configurations and each call
+// picks one from the problem's shape, layout and alignment.  The paper finds
+// that no single configuration wins everywhere and that the best one moves
+// with the problem size (Section 5: the GEMM regions A/B/C on the Mali G-71,
+// and the thread-reuse versus work-group-count trade-off of Section 2.2).
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "../../include/pk.h"
+#include "pk_configs.hpp"
+
+namespace {
+
+using pk::Config;
+using pk::KernelArgs;
+
+// ------------------------------------------------------------ thread state
+
+thread_local int t_last_param = 0;
+thread_local const char *t_last_config = "";
+thread_local const Config *t_forced = nullptr;
+thread_local bool t_forced_set = false;
+thread_local int t_forced_splits = 0;
+
+const Config *env_forced = nullptr;
+bool env_forced_bad = false;
+std::once_flag env_once;
+
+const Config *find_config(const char *name)
+{
+    int n = 0;
+    const Config *cfgs = pk::configs(&n);
+    for (int i = 0; i < n; ++i)
+        if (strcmp(cfgs[i].name, name) == 0) return &cfgs[i];
+    return nullptr;
+}
+
+void read_env()
+{
+    const char *e = getenv("PK_FORCE_CONFIG");
+    if (e && *e) {
+        env_forced = find_config(e);
+        env_forced_bad = env_forced == nullptr;
+    }
+}
+
+// The configuration forced for this call, if any; *bad when the environment
+// names an unknown configuration.
+const Config *forced(bool *bad)
+{
+    std::call_once(env_once, read_env);
+    *bad = false;
+    if (t_forced_set) return t_forced;
+    *bad = env_forced_bad;
+    return env_forced;
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *e = getenv(name);
+    if (!e || !*e) return dflt;
+    return atoi(e);
+}
+
+int invalid(int position)
+{
+    t_last_param = position;
+    return PK_ERR_INVALID_VALUE;
+}
+
+int begin()
+{
+    t_last_param = 0;
+    t_last_config = "";
+    return PK_OK;
+}
+
+int trans_flag(char t)
+{
+    if (t == 'N' || t == 'n') return 0;
+    if (t == 'T' || t == 't' || t == 'C' || t == 'c') return 1;
+    return -1;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Byte range [lo, hi) of a row-major rows x cols matrix with leading dimension ld.
+void span(const float *p, int64_t rows, int64_t cols, int64_t ld, uintptr_t *lo, uintptr_t *hi)
+{
+    *lo = (uintptr_t)p;
+    *hi = (uintptr_t)(p + (rows - 1) * ld + cols);
+}
+
+bool overlap(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a0 < b1 && b0 < a1; }
+
+// a * b * c without overflow, or -1.
+int64_t checked_mul3(int64_t a, int64_t b, int64_t c)
+{
+    int64_t ab, abc;
+    if (__builtin_mul_overflow(a, b, &ab) || __builtin_mul_overflow(ab, c, &abc)) return -1;
+    return abc;
+}
+
+constexpr int64_t kMaxDim = (int64_t)1 << 30;  // kernel tile indexing is 32-bit
+
+// ------------------------------------------------------------ selection
+
+// Number of CUs of MI355X; the work decomposition aims at several
+// work-groups per CU (Section 2.2, thread reusability vs occupancy).
+constexpr int kCUs = 256;
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool gemm_vec_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, const float *A, int64_t lda,
+                 const float *B, int64_t ldb)
+{
+    const bool a_ok = (ta ? M % 4 == 0 : K % 4 == 0) && lda % 4 == 0 && aligned16(A);
+    const bool b_ok = (tb ? K % 4 == 0 : N % 4 == 0) && ldb % 4 == 0 && aligned16(B);
+    return a_ok && b_ok;
+}
+
+bool gemm_config_fits(const Config *c, int ta, int tb, bool vec_ok)
+{
+    if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb) return false;
+    if ((c->vec_a > 1 || c->vec_b > 1) && !vec_ok) return false;
+    return true;
+}
+
+const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, bool vec_ok)
+{
+    int n = 0;
+    const Config *cfgs = pk::configs(&n);
+    int bm = 64, bn = 64, v = 1;
+    if (vec_ok) {
+        v = 4;
+        const int64_t tiles128 = ceil_div(M, 128) * ceil_div(N, 128);
+        if (tiles128 >= kCUs) bm = bn = 128;
+    }
+    for (int i = 0; i < n; ++i) {
+        const Config *c = &cfgs[i];
+        if (c->kind == pk::KIND_GEMM && c->trans_a == ta && c->trans_b == tb && c->bm == bm &&
+            c->bn == bn && c->vec_a == v && c->vec_b == v)
+            return c;
+    }
+    return nullptr;
+}
+
+bool conv_config_fits(const Config *c, bool va4, bool vb4)
+{
+    if (c->kind != pk::KIND_CONV) return false;
+    if (c->vec_a > 1 && !va4) return false;
+    if (c->vec_b > 1 && !vb4) return false;
+    return true;
+}
+
+const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4)
+{
+    const char *name;
+    if (va4 && vb4) {
+        if (Cout <= 64)
+            name = "conv_128x64x16_w2x2_v44";
+        else if (ceil_div(M, 128) * ceil_div(Cout, 128) >= kCUs)
+            name = "conv_128x128x16_w2x2_v44";
+        else
+            name = "conv_64x64x16_w2x2_v44";
+    } else if (vb4) {
+        name = "conv_128x64x16_w2x2_v14";
+    } else {
+        name = "conv_64x64x16_w2x2_v11";
+    }
+    return find_config(name);
+}
+
+// Split of the K reduction when the output alone gives too few work-groups.
+int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
+{
+    const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
+    const int64_t nkb = ceil_div(K, c->bk);
+    if (tiles >= kCUs) return 1;
+    int64_t s = ceil_div(2 * kCUs, tiles);
+    const int64_t max_by_k = nkb / 8;  // keep at least 8 K-blocks per split
+    if (s > max_by_k) s = max_by_k;
+    if (s > 16) s = 16;
+    return s < 1 ? 1 : (int)s;
+}
+
+void fill_common(KernelArgs &a, const Config *c, int64_t M, int64_t N, int64_t K, int splits)
+{
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    a.tiles_m = (int)ceil_div(M, c->bm);
+    a.tiles_n = (int)ceil_div(N, c->bn);
+    const int nkb = (int)ceil_div(K, c->bk);
+    if (splits < 1) splits = 1;
+    if (splits > nkb) splits = nkb > 0 ? nkb : 1;
+    a.kblocks_per_split = (int)ceil_div(nkb, splits);
+    a.splits = (int)ceil_div(nkb, a.kblocks_per_split);
+    if (a.splits < 1) a.splits = 1;
+    a.xcds = env_int("PK_XCDS", 8);
+    if (a.xcds < 1) a.xcds = 1;
+    a.group_m = env_int("PK_GROUP_M", 8);
+    if (a.group_m < 1) a.group_m = 1;
+}
+
+int launch(const Config *c, const KernelArgs &a, hipStream_t stream)
+{
+    if (c->launch(a, stream) != hipSuccess) return PK_ERR_LAUNCH;
+    if (a.splits > 1 &&
+        pk::launch_splitk_reduce(a.ws, a.C, a.M, a.N, a.ldc, a.splits, a.beta, stream) != hipSuccess)
+        return PK_ERR_LAUNCH;
+    t_last_config = c->name;
+    return PK_OK;
+}
+
+int out_dims(int64_t H, int64_t W, int64_t KH, int64_t KW, int64_t sh, int64_t sw, int64_t pt,
+             int64_t pl, int64_t pb, int64_t pr, int64_t *Ho, int64_t *Wo, int first_pos)
+{
+    // first_pos: argument position of H in the caller's signature
+    // (H, W, KH, KW, sh, sw, pt, pl, pb, pr follow the pk_conv2d_out_dims order
+    // when first_pos == 1; pk_conv2d_fwd maps them itself).
+    (void)first_pos;
+    if (H < 1) return invalid(1);
+    if (W < 1) return invalid(2);
+    if (KH < 1) return invalid(3);
+    if (KW < 1) return invalid(4);
+    if (sh < 1) return invalid(5);
+    if (sw < 1) return invalid(6);
+    if (pt < 0) return invalid(7);
+    if (pl < 0) return invalid(8);
+    if (pb < 0) return invalid(9);
+    if (pr < 0) return invalid(10);
+    if (H > kMaxDim || W > kMaxDim || KH > kMaxDim || KW > kMaxDim || pt > kMaxDim || pb > kMaxDim ||
+        pl > kMaxDim || pr > kMaxDim)
+        return PK_ERR_NOT_SUPPORTED;
+    const int64_t hs = H + pt + pb - KH, ws = W + pl + pr - KW;
+    if (hs < 0) return invalid(3);
+    if (ws < 0) return invalid(4);
+    *Ho = hs / sh + 1;
+    *Wo = ws / sw + 1;
+    return PK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *pk_status_string(int status)
+{
+    switch (status) {
+    case PK_OK: return "PK_OK";
+    case PK_ERR_INVALID_VALUE: return "PK_ERR_INVALID_VALUE: an argument is out of range";
+    case PK_ERR_NOT_SUPPORTED: return "PK_ERR_NOT_SUPPORTED: request not implemented";
+    case PK_ERR_WORKSPACE: return "PK_ERR_WORKSPACE: forced split needs more workspace";
+    case PK_ERR_LAUNCH: return "PK_ERR_LAUNCH: the HIP runtime refused a launch";
+    default: return "unknown pk status";
+    }
+}
+
+int pk_last_invalid_param(void) { return t_last_param; }
+
+const char *pk_last_config_name(void) { return t_last_config; }
+
+int pk_num_configs(void)
+{
+    int n = 0;
+    pk::configs(&n);
+    return n;
+}
+
+int pk_get_config(int idx, pk_config_info *info)
+{
+    begin();
+    int n = 0;
+    const Config *cfgs = pk::configs(&n);
+    if (idx < 0 || idx >= n) return invalid(1);
+    if (!info) return invalid(2);
+    const Config *c = &cfgs[idx];
+    info->name = c->name;
+    info->kind = c->kind;
+    info->bm = c->bm;
+    info->bn = c->bn;
+    info->bk = c->bk;
+    info->waves_m = c->waves_m;
+    info->waves_n = c->waves_n;
+    info->threads = 64 * c->waves_m * c->waves_n;
+    info->trans_a = c->trans_a;
+    info->trans_b = c->trans_b;
+    info->vec_a = c->vec_a;
+    info->vec_b = c->vec_b;
+    info->stages = 2;
+    info->lds_bytes = c->lds_bytes;
+    return PK_OK;
+}
+
+int pk_force_config(const char *name)
+{
+    begin();
+    if (!name || !*name) {
+        t_forced = nullptr;
+        t_forced_set = false;
+        return PK_OK;
+    }
+    const Config *c = find_config(name);
+    if (!c) return invalid(1);
+    t_forced = c;
+    t_forced_set = true;
+    return PK_OK;
+}
+
+int pk_force_splits(int splits)
+{
+    begin();
+    if (splits < 0) return invalid(1);
+    t_forced_splits = splits;
+    return PK_OK;
+}
+
+int pk_conv2d_out_dims(int64_t H, int64_t W, int64_t KH, int64_t KW, int64_t sh, int64_t sw,
+                       int64_t pt, int64_t pl, int64_t pb, int64_t pr, int64_t *Ho, int64_t *Wo)
+{
+    begin();
+    if (!Ho) return invalid(11);
+    if (!Wo) return invalid(12);
+    return out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr, Ho, Wo, 1);
+}
+
+int pk_conv2d_same_pads(int64_t H, int64_t W, int64_t KH, int64_t KW, int64_t sh, int64_t sw,
+                        int64_t pads_tlbr[4])
+{
+    begin();
+    if (H < 1) return invalid(1);
+    if (W < 1) return invalid(2);
+    if (KH < 1) return invalid(3);
+    if (KW < 1) return invalid(4);
+    if (sh < 1) return invalid(5);
+    if (sw < 1) return invalid(6);
+    if (!pads_tlbr) return invalid(7);
+    if (H > kMaxDim || W > kMaxDim || KH > kMaxDim || KW > kMaxDim || sh > kMaxDim || sw > kMaxDim)
+        return PK_ERR_NOT_SUPPORTED;
+    const int64_t ho = ceil_div(H, sh), wo = ceil_div(W, sw);
+    int64_t ph = (ho - 1) * sh + KH - H, pw = (wo - 1) * sw + KW - W;
+    if (ph < 0) ph = 0;
+    if (pw < 0) pw = 0;
+    pads_tlbr[0] = ph / 2;
+    pads_tlbr[1] = pw / 2;
+    pads_tlbr[2] = ph - ph / 2;
+    pads_tlbr[3] = pw - pw / 2;
+    return PK_OK;
+}
+
+int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
+             int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, void *stream)
+{
+    begin();
+    const int ta = trans_flag(transA), tb = trans_flag(transB);
+    if (ta < 0) return invalid(1);
+    if (tb < 0) return invalid(2);
+    if (M < 0) return invalid(3);
+    if (N < 0) return invalid(4);
+    if (K < 0) return invalid(5);
+    const int64_t a_cols = ta ? M : K, b_cols = tb ? K : N;
+    if (lda < (a_cols > 1 ? a_cols : 1)) return invalid(8);
+    if (ldb < (b_cols > 1 ? b_cols : 1)) return invalid(10);
+    if (ldc < (N > 1 ? N : 1)) return invalid(13);
+    if (M == 0 || N == 0) return PK_OK;
+    if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return PK_ERR_NOT_SUPPORTED;
+    if (!C) return invalid(12);
+    hipStream_t s = (hipStream_t)stream;
+    uintptr_t c0, c1;
+    span(C, M, N, ldc, &c0, &c1);
+    if (alpha == 0.f || K == 0) {
+        if (pk::launch_scale(C, (int)M, (int)N, ldc, beta, s) != hipSuccess) return PK_ERR_LAUNCH;
+        t_last_config = "scale";
+        return PK_OK;
+    }
+    if (!A) return invalid(7);
+    if (!B) return invalid(9);
+    uintptr_t a0, a1, b0, b1;
+    span(A, ta ? K : M, a_cols, lda, &a0, &a1);
+    span(B, tb ? N : K, b_cols, ldb, &b0, &b1);
+    if (overlap(c0, c1, a0, a1) || overlap(c0, c1, b0, b1)) return invalid(12);
+
+    const bool vec_ok = gemm_vec_ok(ta, tb, M, N, K, A, lda, B, ldb);
+    bool bad = false;
+    const Config *c = forced(&bad);
+    if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
+    if (c) {
+        if (!gemm_config_fits(c, ta, tb, vec_ok)) return PK_ERR_NOT_SUPPORTED;
+    } else {
+        c = select_gemm(ta, tb, M, N, vec_ok);
+        if (!c) return PK_ERR_NOT_SUPPORTED;
+    }
+    KernelArgs a;
+    memset(&a, 0, sizeof(a));
+    a.A = A;
+    a.B = B;
+    a.C = C;
+    a.ws = nullptr;
+    a.lda = lda;
+    a.ldb = ldb;
+    a.ldc = ldc;
+    a.alpha = alpha;
+    a.beta = beta;
+    fill_common(a, c, M, N, K, 1);
+    return launch(c, a, s);
+}
+
+size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, int64_t KH, int64_t KW,
+                                 int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb,
+                                 int64_t pr)
+{
+    int64_t Ho = 0, Wo = 0;
+    if (N < 1 || Cin < 1 || Cout < 1) return 0;
+    const int saved = t_last_param;
+    const int st = out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr, &Ho, &Wo, 2);
+    t_last_param = saved;
+    if (st != PK_OK) return 0;
+    const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
+    if (gemm_path) return 0;
+    const int64_t M = checked_mul3(N, Ho, Wo), K = checked_mul3(KH, KW, Cin);
+    if (M < 0 || K < 0 || M > kMaxDim || K > kMaxDim || Cout > kMaxDim) return 0;
+    const Config *c = select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
+    if (!c) return 0;
+    const int splits = t_forced_splits > 0 ? t_forced_splits : choose_splits(c, M, Cout, K);
+    if (splits <= 1) return 0;
+    return (size_t)splits * (size_t)M * (size_t)Cout * sizeof(float);
+}
+
+int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, const float *f, int64_t KH,
+                  int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb,
+                  int64_t pr, float *y, int64_t Ho, int64_t Wo, void *workspace, size_t workspace_bytes,
+                  void *stream)
+{
+    begin();
+    if (N < 0) return invalid(2);
+    if (H < 1) return invalid(3);
+    if (W < 1) return invalid(4);
+    if (Cin < 1) return invalid(5);
+    if (KH < 1) return invalid(7);
+    if (KW < 1) return invalid(8);
+    if (Cout < 1) return invalid(9);
+    if (sh < 1) return invalid(10);
+    if (sw < 1) return invalid(11);
+    if (pt < 0) return invalid(12);
+    if (pl < 0) return invalid(13);
+    if (pb < 0) return invalid(14);
+    if (pr < 0) return invalid(15);
+    int64_t ho = 0, wo = 0;
+    {
+        const int st = out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr, &ho, &wo, 2);
+        if (st == PK_ERR_INVALID_VALUE) {
+            // map the helper's positions onto this signature
+            static const int map[11] = {0, 3, 4, 7, 8, 10, 11, 12, 13, 14, 15};
+            return invalid(map[t_last_param]);
+        }
+        if (st != PK_OK) return st;
+    }
+    if (Ho != ho) return invalid(17);
+    if (Wo != wo) return invalid(18);
+    if (N == 0) return PK_OK;
+    if (!x) return invalid(1);
+    if (!f) return invalid(6);
+    if (!y) return invalid(16);
+    const int64_t M = checked_mul3(N, Ho, Wo), K = checked_mul3(KH, KW, Cin);
+    const int64_t pixels = checked_mul3(N, H, W);
+    if (M < 0 || K < 0 || pixels < 0 || N > kMaxDim || Cin > kMaxDim || Cout > kMaxDim || M > kMaxDim ||
+        K > kMaxDim || H * W > kMaxDim || checked_mul3(pixels, Cin, 1) < 0 || checked_mul3(K, Cout, 1) < 0 ||
+        checked_mul3(M, Cout, 1) < 0)
+        return PK_ERR_NOT_SUPPORTED;
+    uintptr_t x0, x1, f0, f1, y0, y1;
+    span(x, N * H * W, Cin, Cin, &x0, &x1);
+    span(f, K, Cout, Cout, &f0, &f1);
+    span(y, M, Cout, Cout, &y0, &y1);
+    if (overlap(y0, y1, x0, x1) || overlap(y0, y1, f0, f1)) return invalid(16);
+    hipStream_t s = (hipStream_t)stream;
+
+    KernelArgs a;
+    memset(&a, 0, sizeof(a));
+    a.B = f;
+    a.ldb = Cout;
+    a.C = y;
+    a.ldc = Cout;
+    a.alpha = 1.f;
+    a.beta = 0.f;
+
+    bool bad = false;
+    const Config *c = forced(&bad);
+    if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
+
+    const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
+    if (gemm_path) {
+        // 1x1, stride 1, no padding: the image is already the M x Cin matrix.
+        const bool vec_ok = gemm_vec_ok(0, 0, M, Cout, Cin, x, Cin, f, Cout);
+        if (c) {
+            if (!gemm_config_fits(c, 0, 0, vec_ok)) return PK_ERR_NOT_SUPPORTED;
+        } else {
+            c = select_gemm(0, 0, M, Cout, vec_ok);
+            if (!c) return PK_ERR_NOT_SUPPORTED;
+        }
+        a.A = x;
+        a.lda = Cin;
+        fill_common(a, c, M, Cout, Cin, 1);
+        return launch(c, a, s);
+    }
+
+    const bool va4 = Cin % 4 == 0 && aligned16(x);
+    const bool vb4 = Cout % 4 == 0 && aligned16(f);
+    if (c) {
+        if (!conv_config_fits(c, va4, vb4)) return PK_ERR_NOT_SUPPORTED;
+    } else {
+        c = select_conv(M, Cout, va4, vb4);
+        if (!c) return PK_ERR_NOT_SUPPORTED;
+    }
+    int splits = 1;
+    const size_t per_split = (size_t)M * (size_t)Cout * sizeof(float);
+    if (t_forced_splits > 0) {
+        splits = t_forced_splits;
+        if (splits > 1 && (!workspace || workspace_bytes < (size_t)splits * per_split)) return PK_ERR_WORKSPACE;
+    } else {
+        splits = choose_splits(c, M, Cout, K);
+        if (splits > 1 && (!workspace || workspace_bytes < (size_t)splits * per_split)) splits = 1;
+    }
+    a.A = x;
+    a.lda = Cin;
+    a.H = (int)H;
+    a.W = (int)W;
+    a.Cin = (int)Cin;
+    a.KW = (int)KW;
+    a.sh = (int)sh;
+    a.sw = (int)sw;
+    a.pt = (int)pt;
+    a.pl = (int)pl;
+    a.Ho = (int)Ho;
+    a.Wo = (int)Wo;
+    fill_common(a, c, M, Cout, K, splits);
+    if (a.splits > 1) {
+        uintptr_t w0 = (uintptr_t)workspace, w1 = w0 + (size_t)a.splits * per_split;
+        if (overlap(w0, w1, x0, x1) || overlap(w0, w1, f0, f1) || overlap(w0, w1, y0, y1)) return invalid(19);
+        a.ws = (float *)workspace;
+    }
+    return launch(c, a, s);
+}
+
+}  // extern "C"

@@ -1,0 +1,24 @@
+// pk_args.hpp -- the argument block every contraction kernel receives.
+#pragma once
+
+#include <stdint.h>
+
+namespace pk {
+
+struct KernelArgs {
+    const float *A;  // dense A, or the NHWC image for A_CONV
+    const float *B;  // dense B (for the convolution: the HWIO filter, K x Cout)
+    float *C;
+    float *ws;       // split-K partial sums, splits x M x N (NULL when splits == 1)
+    int M, N, K;
+    int64_t lda, ldb, ldc;
+    float alpha, beta;
+    int tiles_m, tiles_n;
+    int splits, kblocks_per_split;
+    int xcds, group_m;
+    // implicit-GEMM geometry: A(m, k) = x[n][ho*sh - pt + kh][wo*sw - pl + kw][ci]
+    // with m = (n*Ho + ho)*Wo + wo and k = (kh*KW + kw)*Cin + ci.
+    int H, W, Cin, KW, sh, sw, pt, pl, Ho, Wo;
+};
+
+}  // namespace pk

@@ -1,0 +1,480 @@
+// pk_kernel.hpp -- the parameterized fp32 contraction for gfx950.
+//
+// One template computes a BM x BN block of C = alpha * op(A) * op(B) (+ beta C)
+// per work-group, the panel-times-panel decomposition of the blocked GEMM in
+// Section 3.1: C is cut into blocks, each block C_ij is the product of the row
+// panel A_i and the column panel B_j, and the K dimension is walked in blocks
+// of BK (the blocked identity over a partition of K).  The levels of the
+// paper's memory hierarchy map onto CDNA4 as
+//   global (HBM / L2)  ->  LDS (the paper's local memory), double buffered
+//                      ->  VGPRs (private memory)  ->  fp32 MFMA accumulators.
+//
+// Tile parameters (compile time, as the paper's template parameters):
+//   BM, BN      work-group tile of C
+//   BK          K-block depth staged in LDS per step
+//   WAVES_M/N   wave grid; each 64-lane wave owns a (BM/WAVES_M) x (BN/WAVES_N)
+//               sub-tile built from 32 x 32 MFMA blocks
+//   VA, VB      elements per global load (1 or 4: 4 = 16-byte loads)
+//   AMODE       how op(A) is read: dense k-contiguous ('N'), dense
+//               m-contiguous ('T'), or gathered from an NHWC image (implicit
+//               GEMM convolution, k = (kh*KW + kw)*Cin + ci)
+//   B_KCONTIG   op(B) read from N x K storage ('T') instead of K x N ('N')
+//
+// Matrix instruction: v_mfma_f32_32x32x2_f32 (full fp32 products and sums).
+// For one instruction, lane l supplies A(row l%32, k-slot l/32) and
+// B(k-slot l/32, col l%32) and holds 16 results: C(8*(r/4) + 4*(l/32) + r%4,
+// l%32) for r = 0..15.  The two k-slots of the instruction are given the
+// k-indices h*BK/2 + s (h = l/32, s = 0..BK/2-1) of the current K-block, so
+// each lane walks BK/2 consecutive k of its own row: a permutation of the
+// K-block that the sum does not see, but one that lets an A row stored
+// k-contiguous in LDS be read with 16-byte LDS loads.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "pk_args.hpp"
+
+namespace pk {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+enum AMode { A_KCONTIG = 0, A_MCONTIG = 1, A_CONV = 2 };
+
+
+// Maps the linear work-group id to a C tile.  Work-groups are handed to the
+// 8 XCDs round-robin (id % 8); renumbering them so that each XCD receives a
+// contiguous run of logical tiles keeps the A and B panels those tiles share
+// in that XCD's own L2.  Logical tiles are then ordered in column strips of
+// group_m tile-rows so that concurrently running tiles reuse panels.
+__device__ __forceinline__ void tile_coords(const KernelArgs &p, int &tm, int &tn)
+{
+    int pid = blockIdx.x;
+    const int num = p.tiles_m * p.tiles_n;
+    if (p.xcds > 1) {
+        const int q = num / p.xcds, r = num % p.xcds;
+        const int x = pid % p.xcds, loc = pid / p.xcds;
+        pid = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + loc;
+    }
+    const int group = p.group_m * p.tiles_n;
+    const int gid = pid / group;
+    const int first_m = gid * p.group_m;
+    const int gsz = min(p.tiles_m - first_m, p.group_m);
+    const int in_group = pid - gid * group;
+    tm = first_m + in_group % gsz;
+    tn = in_group / gsz;
+}
+
+template <int V>
+struct Vec;
+template <>
+struct Vec<1> {
+    typedef float T;
+    static __device__ __forceinline__ T zero() { return 0.f; }
+    static __device__ __forceinline__ T load(const float *p) { return *p; }
+    static __device__ __forceinline__ void store(float *p, T v) { *p = v; }
+};
+template <>
+struct Vec<4> {
+    typedef f32x4 T;
+    static __device__ __forceinline__ T zero() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+    static __device__ __forceinline__ T load(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
+    static __device__ __forceinline__ void store(float *p, T v) { *reinterpret_cast<f32x4 *>(p) = v; }
+};
+
+// ----------------------------------------------------------------------------
+// Tile loaders: global -> registers (issued one K-block ahead) -> LDS.
+// A loader stages ROWS x COLS of a row-major global panel whose COLS are
+// contiguous.  Thread t owns chunks c = t + i*NT (VEC elements each); since
+// NT is a multiple of the chunks per row, every chunk of a thread sits in the
+// same column, and its row pointer is fixed for the whole K loop.
+// ----------------------------------------------------------------------------
+
+// Dense operand, k along the contiguous columns (A 'N', B 'T').
+// Rows are m (or n); the panel advances along its columns by BK per step.
+template <int ROWS, int BK, int VEC, int NT>
+struct KContigLoader {
+    static constexpr int CPR = BK / VEC;
+    static constexpr int LOADS = ROWS * BK / (VEC * NT);
+    static_assert(NT % CPR == 0, "threads must cover whole rows");
+    static_assert(LOADS >= 1 && ROWS * BK % (VEC * NT) == 0, "tile not divisible");
+    typedef typename Vec<VEC>::T VT;
+    const float *ptr[LOADS];
+    bool row_ok[LOADS];
+    int col;  // k offset of this thread's chunks inside the K-block
+
+    __device__ __forceinline__ void init(const float *base, int64_t ld, int row0, int rows, int kbeg, int tid)
+    {
+        col = (tid % CPR) * VEC;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int r = (tid + i * NT) / CPR;
+            row_ok[i] = row0 + r < rows;
+            const int rr = row_ok[i] ? row0 + r : 0;
+            ptr[i] = base + (int64_t)rr * ld + (int64_t)kbeg * BK + col;
+        }
+    }
+    __device__ __forceinline__ void load(VT *v, int k0, int K) const
+    {
+        const bool k_ok = k0 + col < K;  // VEC divides K whenever VEC > 1
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i)
+            v[i] = (row_ok[i] && k_ok) ? Vec<VEC>::load(ptr[i]) : Vec<VEC>::zero();
+    }
+    __device__ __forceinline__ void advance()
+    {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) ptr[i] += BK;
+    }
+    // LDS tile [ROWS][BK + PAD]
+    template <int LD>
+    __device__ __forceinline__ void store(float *lds, const VT *v, int tid) const
+    {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int r = (tid + i * NT) / CPR;
+            Vec<VEC>::store(lds + r * LD + col, v[i]);
+        }
+    }
+};
+
+// Dense operand whose m (or n) runs along the contiguous columns (A 'T', B 'N').
+// Rows are k; the panel advances by BK rows per step.
+template <int COLS, int BK, int VEC, int NT>
+struct MContigLoader {
+    static constexpr int CPR = COLS / VEC;
+    static constexpr int LOADS = COLS * BK / (VEC * NT);
+    static_assert(NT % CPR == 0 || CPR % NT == 0, "thread/column mapping");
+    static_assert(LOADS >= 1 && COLS * BK % (VEC * NT) == 0, "tile not divisible");
+    typedef typename Vec<VEC>::T VT;
+    const float *ptr;
+    int64_t ld;
+    bool col_ok[LOADS];
+
+    __device__ __forceinline__ void init(const float *base, int64_t ld_, int col0, int cols, int kbeg, int tid)
+    {
+        ld = ld_;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int c = ((tid + i * NT) % CPR) * VEC;
+            col_ok[i] = col0 + c < cols;  // VEC divides cols whenever VEC > 1
+        }
+        ptr = base + (int64_t)kbeg * BK * ld + col0;
+    }
+    __device__ __forceinline__ void load(VT *v, int k0, int K) const
+    {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int c = (tid + i * NT) % CPR * VEC;
+            const int r = (tid + i * NT) / CPR;
+            const bool ok = col_ok[i] && (k0 + r < K);
+            v[i] = ok ? Vec<VEC>::load(ptr + (int64_t)r * ld + c) : Vec<VEC>::zero();
+        }
+    }
+    __device__ __forceinline__ void advance() { ptr += (int64_t)BK * ld; }
+    // LDS tile [BK][COLS + PAD]
+    template <int LD>
+    __device__ __forceinline__ void store(float *lds, const VT *v, int tid) const
+    {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int c = (tid + i * NT) % CPR * VEC;
+            const int r = (tid + i * NT) / CPR;
+            Vec<VEC>::store(lds + r * LD + c, v[i]);
+        }
+    }
+};
+
+// Implicit-GEMM gather of A from an NHWC image: row m is the output pixel
+// (n, ho, wo), column k is the filter tap (kh, kw) and input channel ci.
+// Out-of-image taps read as zero (the zero padding).  With VEC = 4, Cin is a
+// multiple of 4 so a chunk never straddles two taps.
+template <int ROWS, int BK, int VEC, int NT>
+struct ConvGatherLoader {
+    static constexpr int CPR = BK / VEC;
+    static constexpr int LOADS = ROWS * BK / (VEC * NT);
+    static_assert(NT % CPR == 0, "threads must cover whole rows");
+    static_assert(LOADS >= 1 && ROWS * BK % (VEC * NT) == 0, "tile not divisible");
+    typedef typename Vec<VEC>::T VT;
+    const float *img[LOADS];  // start of image n
+    int ih0[LOADS], iw0[LOADS];
+    int col;
+    int ci, kw, kh;  // decomposition of this thread's current k
+    int H, W, Cin, KW;
+
+    __device__ __forceinline__ void init(const KernelArgs &p, int row0, int kbeg, int tid)
+    {
+        H = p.H; W = p.W; Cin = p.Cin; KW = p.KW;
+        col = (tid % CPR) * VEC;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int m = row0 + (tid + i * NT) / CPR;
+            if (m < p.M) {
+                const int wo = m % p.Wo;
+                const int t = m / p.Wo;
+                const int ho = t % p.Ho;
+                const int n = t / p.Ho;
+                img[i] = p.A + (int64_t)n * H * W * Cin;
+                ih0[i] = ho * p.sh - p.pt;
+                iw0[i] = wo * p.sw - p.pl;
+            } else {
+                img[i] = p.A;
+                ih0[i] = -(1 << 28);  // every tap falls outside the image
+                iw0[i] = 0;
+            }
+        }
+        const int k = kbeg * BK + col;
+        const int tap = k / Cin;
+        ci = k - tap * Cin;
+        kh = tap / KW;
+        kw = tap - kh * KW;
+    }
+    __device__ __forceinline__ void load(VT *v, int k0, int K) const
+    {
+        const bool k_ok = k0 + col < K;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int ih = ih0[i] + kh, iw = iw0[i] + kw;
+            const bool ok = k_ok && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
+            v[i] = ok ? Vec<VEC>::load(img[i] + ((int64_t)(ih * W + iw) * Cin + ci)) : Vec<VEC>::zero();
+        }
+    }
+    __device__ __forceinline__ void advance()
+    {
+        ci += BK;
+        while (ci >= Cin) {
+            ci -= Cin;
+            if (++kw == KW) { kw = 0; ++kh; }
+        }
+    }
+    template <int LD>
+    __device__ __forceinline__ void store(float *lds, const VT *v, int tid) const
+    {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int r = (tid + i * NT) / CPR;
+            Vec<VEC>::store(lds + r * LD + col, v[i]);
+        }
+    }
+};
+
+template <int AMODE, int BM, int BK, int VA, int NT>
+struct ALoaderSel;
+template <int BM, int BK, int VA, int NT>
+struct ALoaderSel<A_KCONTIG, BM, BK, VA, NT> { typedef KContigLoader<BM, BK, VA, NT> T; };
+template <int BM, int BK, int VA, int NT>
+struct ALoaderSel<A_MCONTIG, BM, BK, VA, NT> { typedef MContigLoader<BM, BK, VA, NT> T; };
+template <int BM, int BK, int VA, int NT>
+struct ALoaderSel<A_CONV, BM, BK, VA, NT> { typedef ConvGatherLoader<BM, BK, VA, NT> T; };
+
+// LDS padding (floats) appended to each LDS row: keeps rows 16-byte aligned
+// and staggers banks between the two k-halves and between rows.
+constexpr int LDS_PAD = 4;
+
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB>
+struct GemmTile {
+    static constexpr int NT = 64 * WAVES_M * WAVES_N;
+    static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    static constexpr int RM = WM / 32, RN = WN / 32;
+    static constexpr bool A_K = AMODE != A_MCONTIG;  // A staged k-contiguous
+    static constexpr int LDA_S = A_K ? BK + LDS_PAD : BM + LDS_PAD;
+    static constexpr int LDB_S = B_KCONTIG ? BK + LDS_PAD : BN + LDS_PAD;
+    static constexpr int A_STAGE = A_K ? BM * LDA_S : BK * LDA_S;
+    static constexpr int B_STAGE = B_KCONTIG ? BN * LDB_S : BK * LDB_S;
+    static constexpr int LDS_FLOATS = 2 * (A_STAGE + B_STAGE);
+    static constexpr int HALF = BK / 2;
+    static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile is made of 32x32 blocks");
+    static_assert(BK % 8 == 0, "BK must be a multiple of 8");
+};
+
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N)
+gemm_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
+    constexpr int NT = G::NT;
+    typedef typename ALoaderSel<AMODE, BM, BK, VA, NT>::T ALoader;
+    typedef typename std::conditional<B_KCONTIG, KContigLoader<BN, BK, VB, NT>,
+                                      MContigLoader<BN, BK, VB, NT>>::type BLoader;
+
+    __shared__ __attribute__((aligned(16))) float smem[G::LDS_FLOATS];
+    float *As = smem;                      // [2][A_STAGE]
+    float *Bs = smem + 2 * G::A_STAGE;     // [2][B_STAGE]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+
+    int tm, tn;
+    tile_coords(p, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const int nkb = (p.K + BK - 1) / BK;
+    const int kbeg = blockIdx.z * p.kblocks_per_split;
+    const int kend = min(nkb, kbeg + p.kblocks_per_split);
+
+    ALoader la;
+    BLoader lb;
+    if constexpr (AMODE == A_CONV)
+        la.init(p, m0, kbeg, tid);
+    else
+        la.init(p.A, p.lda, m0, p.M, kbeg, tid);
+    lb.init(p.B, p.ldb, n0, p.N, kbeg, tid);
+
+    f32x16 acc[G::RM][G::RN];
+#pragma unroll
+    for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    typename ALoader::VT ra[ALoader::LOADS];
+    typename BLoader::VT rb[BLoader::LOADS];
+
+    if (kbeg < kend) {
+        la.load(ra, kbeg * BK, p.K);
+        lb.load(rb, kbeg * BK, p.K);
+        la.advance();
+        lb.advance();
+        la.template store<G::LDA_S>(As, ra, tid);
+        lb.template store<G::LDB_S>(Bs, rb, tid);
+    }
+    __syncthreads();
+
+    // Fragment addressing (per lane) inside one stage.
+    // A staged k-contiguous: row (wm*WM + i*32 + l32), k from h*HALF.
+    // A staged m-contiguous: element [k][wm*WM + i*32 + l32].
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+
+    int stage = 0;
+    for (int kb = kbeg; kb < kend; ++kb) {
+        const bool more = kb + 1 < kend;
+        if (more) {
+            la.load(ra, (kb + 1) * BK, p.K);
+            lb.load(rb, (kb + 1) * BK, p.K);
+            la.advance();
+            lb.advance();
+        }
+        const float *as = As + stage * G::A_STAGE;
+        const float *bs = Bs + stage * G::B_STAGE;
+#pragma unroll
+        for (int s4 = 0; s4 < G::HALF; s4 += 4) {
+            float fa[G::RM][4], fb[G::RN][4];
+#pragma unroll
+            for (int i = 0; i < G::RM; ++i) {
+                if constexpr (G::A_K) {
+                    const f32x4 v = *reinterpret_cast<const f32x4 *>(
+                        as + (a_row + i * 32) * G::LDA_S + h * G::HALF + s4);
+                    fa[i][0] = v[0]; fa[i][1] = v[1]; fa[i][2] = v[2]; fa[i][3] = v[3];
+                } else {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        fa[i][t] = as[(h * G::HALF + s4 + t) * G::LDA_S + a_row + i * 32];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < G::RN; ++j) {
+                if constexpr (B_KCONTIG) {
+                    const f32x4 v = *reinterpret_cast<const f32x4 *>(
+                        bs + (b_row + j * 32) * G::LDB_S + h * G::HALF + s4);
+                    fb[j][0] = v[0]; fb[j][1] = v[1]; fb[j][2] = v[2]; fb[j][3] = v[3];
+                } else {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        fb[j][t] = bs[(h * G::HALF + s4 + t) * G::LDB_S + b_row + j * 32];
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                    for (int j = 0; j < G::RN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][t], fb[j][t], acc[i][j], 0, 0, 0);
+        }
+        if (more) {
+            la.template store<G::LDA_S>(As + (stage ^ 1) * G::A_STAGE, ra, tid);
+            lb.template store<G::LDB_S>(Bs + (stage ^ 1) * G::B_STAGE, rb, tid);
+        }
+        __syncthreads();
+        stage ^= 1;
+    }
+
+    // Epilogue: C = alpha * acc (+ beta * C), or the split's partial sum.
+    const int col_base = n0 + wn * G::WN + l32;
+    const int row_base = m0 + wm * G::WM + 4 * h;
+    if (p.splits > 1) {
+        float *out = p.ws + (int64_t)blockIdx.z * p.M * p.N;
+#pragma unroll
+        for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                if (row < p.M) {
+#pragma unroll
+                    for (int j = 0; j < G::RN; ++j) {
+                        const int col = col_base + j * 32;
+                        if (col < p.N) out[(int64_t)row * p.N + col] = p.alpha * acc[i][j][r];
+                    }
+                }
+            }
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+            if (row < p.M) {
+                float *crow = p.C + (int64_t)row * p.ldc;
+#pragma unroll
+                for (int j = 0; j < G::RN; ++j) {
+                    const int col = col_base + j * 32;
+                    if (col < p.N) {
+                        float v = p.alpha * acc[i][j][r];
+                        if (p.beta != 0.f) v = fmaf(p.beta, crow[col], v);
+                        crow[col] = v;
+                    }
+                }
+            }
+        }
+}
+
+// Fixed-order reduction of split-K partials: C = sum_z ws[z] (+ beta * C).
+// Element e of the M x N result is summed over z = 0, 1, ... in that order,
+// so the result does not depend on scheduling.
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(const float *ws, float *C, int M, int N,
+                                                            int64_t ldc, int splits, float beta)
+{
+    const int64_t total = (int64_t)M * N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
+        float s = ws[e];
+        for (int z = 1; z < splits; ++z) s += ws[e + z * total];
+        const int64_t row = e / N, col = e - row * N;
+        float *c = C + row * ldc + col;
+        *c = beta != 0.f ? fmaf(beta, *c, s) : s;
+    }
+}
+
+// C <- beta * C (alpha == 0 or K == 0).  beta == 0 writes zeros without reading.
+__global__ void __launch_bounds__(256) scale_kernel(float *C, int M, int N, int64_t ldc, float beta)
+{
+    const int64_t total = (int64_t)M * N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
+        const int64_t row = e / N, col = e - row * N;
+        float *c = C + row * ldc + col;
+        *c = beta != 0.f ? beta * *c : 0.f;
+    }
+}
+
+}  // namespace pk

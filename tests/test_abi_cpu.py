@@ -1,0 +1,153 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+its host-side logic (argument checks, output sizes, padding, the compiled
+tile-parameter space) behaves as documented.  No call here reaches the GPU:
+every call either is host-only or fails validation before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from tests import pins
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pk.h")
+
+
+@pytest.fixture(scope="module")
+def pk():
+    import paper_1904_05347_amd as pk
+    from paper_1904_05347_amd import binding
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_1904_05347_amd import build
+        build.build(verbose=False)
+    pk.load()
+    return pk
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pk_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(pk):
+    from paper_1904_05347_amd import binding
+    names = declared_functions()
+    assert len(names) >= 10
+    lib = ctypes.CDLL(binding.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(binding.SIGNATURES), "binding and header disagree"
+
+
+def test_out_dims_and_same_pads_match_oracle_and_tables(pk):
+    for name in ("vgg16_layers.csv", "resnet50_layers.csv"):
+        for row in pins.read_golden(name):
+            k, s = int(row["window"]), int(row["stride"])
+            H, W = int(row["in_h"]), int(row["in_w"])
+            pads = (0, 0, 0, 0) if k == 7 else pk.conv2d_same_pads(H, W, k, k, s, s)
+            assert pads == ((0, 0, 0, 0) if k == 7 else oracle.same_pads(H, W, k, k, s, s))
+            assert pk.conv2d_out_dims(H, W, k, k, s, s, *pads) == (int(row["out_h"]), int(row["out_w"]))
+    for H in range(1, 10):
+        for k in range(1, 6):
+            for s in range(1, 4):
+                assert pk.conv2d_same_pads(H, H + 2, k, k, s, s) == oracle.same_pads(H, H + 2, k, k, s, s)
+                for pads in [(0, 0, 0, 0), (1, 2, 0, 1), (2, 2, 2, 2)]:
+                    try:
+                        want = oracle.conv2d_out_dims(H, H + 2, k, k, s, s, *pads)
+                    except ValueError:
+                        with pytest.raises(pk.PkError):
+                            pk.conv2d_out_dims(H, H + 2, k, k, s, s, *pads)
+                        continue
+                    assert pk.conv2d_out_dims(H, H + 2, k, k, s, s, *pads) == want
+
+
+def _gemm_status(pk, *args):
+    from paper_1904_05347_amd import binding
+    st = binding.sgemm(*args)
+    return st, pk.last_invalid_param()
+
+
+def test_gemm_argument_checks(pk):
+    fake = 0x10000  # never dereferenced: every call below fails validation or is empty
+    ok = ("N", "N", 4, 5, 6, 1.0, fake, 6, fake + 4096, 5, 0.0, fake + 8192, 5)
+    cases = [
+        ((b"X",) + ok[1:], 1),
+        (ok[:1] + (b"Q",) + ok[2:], 2),
+        (ok[:2] + (-1,) + ok[3:], 3),
+        (ok[:3] + (-1,) + ok[4:], 4),
+        (ok[:4] + (-1,) + ok[5:], 5),
+        (ok[:7] + (5,) + ok[8:], 8),     # lda < K
+        (ok[:9] + (4,) + ok[10:], 10),   # ldb < N
+        (ok[:12] + (4,), 13),            # ldc < N
+        (("T",) + ok[1:7] + (3,) + ok[8:], 8),   # 'T': lda < M
+        (ok[:1] + ("T",) + ok[2:9] + (5,) + ok[10:], 10),  # 'T': ldb < K
+        (ok[:11] + (None,) + ok[12:], 12),       # C missing
+        (ok[:6] + (None,) + ok[7:], 7),          # A missing
+        (ok[:8] + (None,) + ok[9:], 9),          # B missing
+        (ok[:11] + (fake + 16,) + ok[12:], 12),  # C overlaps A
+    ]
+    for args, pos in cases:
+        st, p = _gemm_status(pk, *args)
+        assert (st, p) == (1, pos), (args, st, p)
+    # empty problems return before touching anything
+    assert _gemm_status(pk, "N", "N", 0, 5, 6, 1.0, None, 6, None, 5, 0.0, None, 5)[0] == 0
+    assert _gemm_status(pk, "n", "c", 4, 0, 6, 1.0, None, 6, None, 6, 0.0, None, 1)[0] == 0
+
+
+def test_conv_argument_checks(pk):
+    from paper_1904_05347_amd import binding
+    fake = 0x10000
+    good = dict(x=fake, N=1, H=5, W=5, Cin=4, f=fake + (1 << 20), KH=3, KW=3, Cout=4, sh=1, sw=1,
+                pt=1, pl=1, pb=1, pr=1, y=fake + (2 << 20), Ho=5, Wo=5)
+    order = list(good)
+    bad = [("N", -1, 2), ("H", 0, 3), ("W", 0, 4), ("Cin", 0, 5), ("KH", 0, 7), ("KW", 0, 8),
+           ("Cout", 0, 9), ("sh", 0, 10), ("sw", 0, 11), ("pt", -1, 12), ("pl", -1, 13),
+           ("pb", -1, 14), ("pr", -1, 15), ("Ho", 4, 17), ("Wo", 6, 18), ("KH", 9, 7), ("KW", 8, 8),
+           ("x", None, 1), ("f", None, 6), ("y", None, 16), ("y", fake + 64, 16)]
+    for key, val, pos in bad:
+        args = dict(good)
+        args[key] = val
+        st = binding.conv2d_fwd_raw(*[args[k] for k in order])
+        assert (st, pk.last_invalid_param()) == (1, pos), (key, val, st, pk.last_invalid_param())
+    args = dict(good, N=0)
+    assert binding.conv2d_fwd_raw(*[args[k] for k in order]) == 0
+
+
+def test_config_space(pk):
+    cfgs = pk.configs()
+    assert len(cfgs) >= 10
+    names = [c["name"] for c in cfgs]
+    assert len(set(names)) == len(names)
+    for c in cfgs:
+        assert c["threads"] == 64 * c["waves_m"] * c["waves_n"]
+        assert c["bm"] % (32 * c["waves_m"]) == 0 and c["bn"] % (32 * c["waves_n"]) == 0
+        assert c["bk"] % 8 == 0
+        assert c["stages"] == 2
+        # two LDS stages of the A and B tiles, each row padded by 4 floats
+        a_k = c["kind"] == 1 or not c["trans_a"]
+        a_tile = c["bm"] * (c["bk"] + 4) if a_k else c["bk"] * (c["bm"] + 4)
+        b_tile = c["bn"] * (c["bk"] + 4) if c["trans_b"] else c["bk"] * (c["bn"] + 4)
+        assert c["lds_bytes"] == 2 * 4 * (a_tile + b_tile), c["name"]
+        assert c["lds_bytes"] <= 160 * 1024
+    # every GEMM layout has a 16-byte and a scalar-load instance
+    for ta in (0, 1):
+        for tb in (0, 1):
+            vecs = {c["vec_a"] for c in cfgs if c["kind"] == 0 and c["trans_a"] == ta and c["trans_b"] == tb}
+            assert {1, 4} <= vecs
+
+
+def test_force_config_and_status_strings(pk):
+    from paper_1904_05347_amd import binding
+    with pytest.raises(pk.PkError):
+        pk.force_config("no_such_config")
+    pk.force_config(pk.configs()[0]["name"])
+    pk.force_config(None)
+    with pytest.raises(pk.PkError):
+        pk.force_splits(-1)
+    lib = binding.load()
+    for s in range(5):
+        assert lib.pk_status_string(s)
+    assert pk.conv2d_workspace_bytes(32, 7, 7, 2048, 3, 3, 512, 1, 1, 1, 1, 1, 1) >= 0

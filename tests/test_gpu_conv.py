@@ -1,0 +1,144 @@
+"""Convolution forward on the GPU through the C-ABI against the CPU oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1904_05347_amd import workloads as wl
+from tests.gpu_util import assert_parity, dev, host, require_gpu, sample_conv_outputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(pk, x, f, stride, pads, workspace=None, force=None, splits=0):
+    if force:
+        pk.force_config(force)
+    if splits:
+        pk.force_splits(splits)
+    try:
+        y = pk.conv2d_fwd(dev(x), dev(f), stride=stride, padding=pads, workspace=workspace)
+    finally:
+        if force:
+            pk.force_config(None)
+        if splits:
+            pk.force_splits(0)
+    return host(y), pk.last_config_name()
+
+
+def test_conv_b1_56x56x64_whole_output():
+    torch, pk = require_gpu()
+    case = wl.CONV_SMALL
+    x, f = case.inputs()
+    out, cfg = _run(pk, x, f, case.stride, case.pads)
+    ref, scale = oracle.conv2d(x, f, case.stride, case.pads)
+    assert out.shape == ref.shape == (1, 56, 56, 64)
+    mx = assert_parity(out, ref, scale, case.name + " " + cfg)
+    assert mx < 1e-6
+
+
+def test_conv_b1_integer_exact():
+    torch, pk = require_gpu()
+    case = wl.CONV_SMALL
+    x, f = case.inputs(kind="int")
+    out, cfg = _run(pk, x, f, case.stride, case.pads)
+    ref, _ = oracle.conv2d(x, f, case.stride, case.pads)
+    assert np.array_equal(out.astype(np.float64), ref), cfg
+
+
+SMALL_GEOMS = [
+    # (N, H, W, Cin, KH, KW, Cout, stride, pads)
+    (2, 9, 7, 8, 3, 3, 12, (1, 1), (1, 1, 1, 1)),
+    (1, 13, 11, 4, 3, 3, 68, (2, 2), (0, 0, 1, 1)),
+    (3, 8, 8, 3, 3, 3, 64, (1, 1), (1, 1, 1, 1)),       # Cin = 3: scalar gather
+    (2, 10, 10, 3, 7, 7, 16, (2, 2), (3, 3, 3, 3)),     # 7x7 stride 2
+    (1, 12, 9, 16, 1, 1, 20, (2, 2), (0, 0, 0, 0)),     # 1x1 stride 2: row gather
+    (2, 7, 7, 36, 1, 1, 132, (1, 1), (0, 0, 0, 0)),     # 1x1 stride 1: plain GEMM
+    (1, 6, 5, 5, 2, 3, 7, (1, 2), (1, 0, 0, 2)),        # odd everything: scalar B too
+    (1, 5, 5, 12, 5, 5, 8, (1, 1), (0, 0, 0, 0)),       # window = image
+]
+
+
+@pytest.mark.parametrize("geom", SMALL_GEOMS, ids=lambda g: "x".join(map(str, g[:7])) + "_s%d%d" % g[7])
+def test_conv_small_geometries(geom):
+    torch, pk = require_gpu()
+    N, H, W, Cin, KH, KW, Cout, stride, pads = geom
+    rng = np.random.default_rng(sum(geom[:7]))
+    x = wl.uniform(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+    f = wl.uniform(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
+    out, cfg = _run(pk, x, f, stride, pads)
+    ref, scale = oracle.conv2d(x, f, stride, pads)
+    assert out.shape == ref.shape
+    assert_parity(out, ref, scale, str(geom) + " " + cfg)
+    xi = wl.integers(rng, x.size).reshape(x.shape)
+    fi = wl.integers(rng, f.size).reshape(f.shape)
+    out, cfg = _run(pk, xi, fi, stride, pads)
+    ref, _ = oracle.conv2d(xi, fi, stride, pads)
+    assert np.array_equal(out.astype(np.float64), ref), (geom, cfg)
+
+
+def test_every_conv_config_forced():
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(77)
+    x = wl.integers(rng, 2 * 11 * 10 * 8).reshape(2, 11, 10, 8)
+    f = wl.integers(rng, 3 * 3 * 8 * 20).reshape(3, 3, 8, 20)
+    ref, _ = oracle.conv2d(x, f, (1, 1), (1, 1, 1, 1))
+    for cfg in pk.configs():
+        if cfg["kind"] != 1:
+            continue
+        out, used = _run(pk, x, f, (1, 1), (1, 1, 1, 1), force=cfg["name"])
+        assert used == cfg["name"]
+        assert np.array_equal(out.astype(np.float64), ref), cfg["name"]
+
+
+@pytest.mark.parametrize("splits", [2, 3, 5])
+def test_conv_split_k_forced(splits):
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(splits)
+    N, H, W, Cin, Cout = 1, 9, 9, 64, 96
+    x = wl.uniform(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+    f = wl.uniform(rng, 9 * Cin * Cout).reshape(3, 3, Cin, Cout)
+    ws = torch.empty(splits * N * H * W * Cout, dtype=torch.float32, device="cuda")
+    outs = []
+    for _ in range(2):
+        out, cfg = _run(pk, x, f, (1, 1), (1, 1, 1, 1), workspace=ws, splits=splits)
+        outs.append(out)
+    assert np.array_equal(outs[0], outs[1]), "split-K must be deterministic"
+    ref, scale = oracle.conv2d(x, f, (1, 1), (1, 1, 1, 1))
+    assert_parity(outs[0], ref, scale, "split %d %s" % (splits, cfg))
+    # too little workspace for a forced split is an error, not a silent fallback
+    with pytest.raises(pk.PkError):
+        _run(pk, x, f, (1, 1), (1, 1, 1, 1), workspace=ws[: N * H * W * Cout], splits=splits)
+
+
+@pytest.mark.parametrize("case", wl.VGG_LAYERS + wl.RESNET_LAYERS + [wl.RESNET_ALT], ids=lambda c: c.name)
+def test_conv_layers_sampled(case):
+    """Each layer at batch 32, in the launch configuration the benchmark times."""
+    torch, pk = require_gpu()
+    x, f = case.inputs()
+    N, H, W, Cin = case.x_shape
+    KH, KW, _, Cout = case.f_shape
+    wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
+    ws = torch.empty(max(wsb // 4, 1), dtype=torch.float32, device="cuda") if wsb else None
+    out, cfg = _run(pk, x, f, case.stride, case.pads, workspace=ws)
+    Ho, Wo = case.out_hw
+    assert out.shape == (N, Ho, Wo, Cout)
+    idx = sample_conv_outputs(N, Ho, Wo, Cout, 3000, case.seed)
+    ref, scale = oracle.conv2d_at(x, f, case.stride, case.pads, idx)
+    mx = assert_parity(out.reshape(-1)[idx], ref, scale, case.name + " " + cfg)
+    assert mx < 1e-6
+    assert np.all(np.isfinite(out))
+
+
+def test_conv_batch_zero_and_errors():
+    torch, pk = require_gpu()
+    x = torch.zeros((0, 5, 5, 4), dtype=torch.float32, device="cuda")
+    f = torch.zeros((3, 3, 4, 4), dtype=torch.float32, device="cuda")
+    y = pk.conv2d_fwd(x, f, padding="SAME")
+    assert tuple(y.shape) == (0, 5, 5, 4)
+    xx = torch.zeros((1, 5, 5, 4), dtype=torch.float32, device="cuda")
+    yy = torch.zeros((1, 5, 5, 4), dtype=torch.float32, device="cuda")
+    st = pk.binding.conv2d_fwd_raw(xx.data_ptr(), 1, 5, 5, 4, f.data_ptr(), 3, 3, 4, 1, 1, 1, 1, 1, 1,
+                                   yy.data_ptr(), 4, 5)  # wrong Ho
+    assert st == 1 and pk.last_invalid_param() == 17
+    st = pk.binding.conv2d_fwd_raw(xx.data_ptr(), 1, 5, 5, 4, f.data_ptr(), 3, 3, 4, 1, 1, 1, 1, 1, 1,
+                                   xx.data_ptr(), 5, 5)  # output aliases input
+    assert st == 1 and pk.last_invalid_param() == 16

@@ -1,0 +1,179 @@
+"""GEMM on the GPU through the C-ABI against the CPU oracle."""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1904_05347_amd import workloads as wl
+from tests.gpu_util import assert_parity, dev, host, require_gpu, sample_rows_cols
+
+pytestmark = pytest.mark.gpu
+
+
+def _gemm_case(torch, pk, ta, tb, M, N, K, alpha, beta, seed, kind="uniform", slack=0, force=None):
+    rng = np.random.default_rng(seed)
+    draw = wl.uniform if kind == "uniform" else wl.integers
+    a_rows, a_cols = (K, M) if ta == "T" else (M, K)
+    b_rows, b_cols = (N, K) if tb == "T" else (K, N)
+    A = draw(rng, a_rows * (a_cols + slack)).reshape(a_rows, a_cols + slack)
+    B = draw(rng, b_rows * (b_cols + slack)).reshape(b_rows, b_cols + slack)
+    C = draw(rng, M * (N + slack)).reshape(M, N + slack)
+    dA, dB, dC = dev(A), dev(B), dev(C)
+    if force:
+        pk.force_config(force)
+    try:
+        st = pk.binding.sgemm(ta, tb, M, N, K, alpha, dA.data_ptr(), A.shape[1], dB.data_ptr(), B.shape[1],
+                              beta, dC.data_ptr(), C.shape[1], torch.cuda.current_stream().cuda_stream)
+    finally:
+        if force:
+            pk.force_config(None)
+    assert st == 0, (st, pk.last_invalid_param())
+    cfg = pk.last_config_name()
+    out = host(dC)
+    ref, scale = oracle.sgemm(ta, tb, M, N, K, alpha, A, A.shape[1], B, B.shape[1], beta, C, C.shape[1])
+    # the slack columns of C must be untouched
+    assert np.array_equal(out[:, N:], C[:, N:])
+    return out[:, :N], ref, scale, C[:, :N], cfg
+
+
+def test_gemm_512_parity():
+    torch, pk = require_gpu()
+    case = wl.GEMM_SMALL
+    A, B, C = case.inputs()
+    C = np.full_like(C, np.nan)  # beta == 0: C must not be read
+    dA, dB, dC = dev(A), dev(B), dev(C)
+    pk.gemm(dA, dB, dC, alpha=1.0, beta=0.0)
+    out = host(dC)
+    ref, scale = oracle.sgemm("N", "N", 512, 512, 512, 1.0, A, 512, B, 512, 0.0, C, 512)
+    mx = assert_parity(out, ref, scale, case.name)
+    assert mx < 1e-6
+
+
+def test_gemm_512_integer_exact():
+    torch, pk = require_gpu()
+    out, ref, _, _, cfg = _gemm_case(torch, pk, "N", "N", 512, 512, 512, 1.0, 0.0, 101, kind="int")
+    assert np.array_equal(out.astype(np.float64), ref), cfg
+
+
+@pytest.mark.parametrize("ta,tb", list(itertools.product("NT", "NT")))
+def test_gemm_transposes_integer_exact(ta, tb):
+    torch, pk = require_gpu()
+    # several tiles plus ragged tails in M and N; K a multiple of 4 (16-byte path)
+    out, ref, _, _, cfg = _gemm_case(torch, pk, ta, tb, 300, 268, 132, 1.0, 0.5, 7, kind="int")
+    assert np.array_equal(out.astype(np.float64), ref), (ta, tb, cfg)
+
+
+EDGE = [1, 3, 17, 63, 65, 129]
+
+
+@pytest.mark.parametrize("ta,tb", list(itertools.product("NT", "NT")))
+def test_gemm_edge_shapes(ta, tb):
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(hash((ta, tb)) % 1000)
+    shapes = [(m, n, k) for m in EDGE for n in EDGE for k in (1, 2, 17, 65)]
+    picks = [shapes[i] for i in rng.choice(len(shapes), 24, replace=False)] + [(129, 129, 129), (1, 1, 1)]
+    for M, N, K in picks:
+        out, ref, scale, C, cfg = _gemm_case(torch, pk, ta, tb, M, N, K, 1.5, -0.5, M * 7 + N * 3 + K, slack=3)
+        assert_parity(out, ref, scale, "%s%s %dx%dx%d %s" % (ta, tb, M, N, K, cfg),
+                      extra=np.abs(0.5 * C.astype(np.float64)))
+
+
+def test_gemm_quick_returns():
+    torch, pk = require_gpu()
+    M, N, K = 70, 33, 20
+    rng = np.random.default_rng(5)
+    A = wl.uniform(rng, M * K).reshape(M, K)
+    B = wl.uniform(rng, K * N).reshape(K, N)
+    C = wl.uniform(rng, M * N).reshape(M, N)
+    # alpha == 0: C <- beta C, A/B not read (NaN there must not leak)
+    dA = dev(np.full_like(A, np.nan))
+    dB = dev(np.full_like(B, np.nan))
+    dC = dev(C)
+    pk.gemm(dA, dB, dC, alpha=0.0, beta=0.5)
+    assert np.array_equal(host(dC), (C * np.float32(0.5)))
+    # K == 0: C <- beta C
+    dC = dev(C)
+    st = pk.binding.sgemm("N", "N", M, N, 0, 1.0, None, 1, None, N, 2.0, dC.data_ptr(), N)
+    assert st == 0
+    assert np.array_equal(host(dC), C * np.float32(2.0))
+    # beta == 0 with alpha == 0 writes zeros even over NaN
+    dC = dev(np.full_like(C, np.nan))
+    pk.gemm(dev(A), dev(B), dC, alpha=0.0, beta=0.0)
+    assert np.array_equal(host(dC), np.zeros_like(C))
+    # M == 0 / N == 0: nothing happens
+    assert pk.binding.sgemm("N", "N", 0, N, K, 1.0, None, K, None, N, 0.0, None, N) == 0
+    assert pk.binding.sgemm("N", "N", M, 0, K, 1.0, None, K, None, 1, 0.0, None, 1) == 0
+
+
+def test_gemm_deterministic_and_streams():
+    torch, pk = require_gpu()
+    case = wl.GEMM_SWEEP[0]
+    A, B, C = case.inputs()
+    dA, dB = dev(A), dev(B)
+    outs = []
+    s = torch.cuda.Stream()
+    for stream in (None, s):
+        dC = dev(C)
+        if stream is None:
+            pk.gemm(dA, dB, dC, alpha=1.0, beta=0.5)
+        else:
+            stream.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(stream):
+                pk.gemm(dA, dB, dC, alpha=1.0, beta=0.5)
+            torch.cuda.current_stream().wait_stream(stream)
+        outs.append(host(dC))
+    assert np.array_equal(outs[0], outs[1])
+    rows, cols = sample_rows_cols(1024, 1024, 2000, 3)
+    ref, scale = oracle.sgemm_at("N", "N", 1024, 1024, 1024, 1.0, A, 1024, B, 1024, 0.5, C, 1024, rows, cols)
+    assert_parity(outs[0][rows, cols], ref, scale, case.name)
+
+
+@pytest.mark.parametrize("case", wl.GEMM_SWEEP, ids=lambda c: c.name)
+def test_gemm_sweep_sampled(case):
+    """The sweep at full size, in the launch configuration the benchmark times."""
+    torch, pk = require_gpu()
+    A, B, C = case.inputs()
+    dA, dB, dC = dev(A), dev(B), dev(C)
+    pk.gemm(dA, dB, dC, alpha=case.alpha, beta=case.beta,
+            trans_a=case.trans_a == "T", trans_b=case.trans_b == "T")
+    out = host(dC)
+    rows, cols = sample_rows_cols(case.M, case.N, 3000, case.seed)
+    ref, scale = oracle.sgemm_at(case.trans_a, case.trans_b, case.M, case.N, case.K, case.alpha,
+                                 A, case.lda, B, case.ldb, case.beta, C, case.ldc, rows, cols)
+    mx = assert_parity(out[rows, cols], ref, scale, case.name + " " + pk.last_config_name())
+    assert mx < 1e-6
+    # every output is finite and was written (C held values in [-1, 1); the
+    # product terms reach |sum| >> 1 for most entries)
+    assert np.all(np.isfinite(out))
+
+
+def test_every_gemm_config_forced():
+    torch, pk = require_gpu()
+    for cfg in pk.configs():
+        if cfg["kind"] != 0:
+            continue
+        ta = "T" if cfg["trans_a"] else "N"
+        tb = "T" if cfg["trans_b"] else "N"
+        for M, N, K in [(200, 136, 72), (64, 64, 16), (4, 260, 36)]:
+            out, ref, scale, C, used = _gemm_case(torch, pk, ta, tb, M, N, K, 1.0, 0.5, M + N + K,
+                                                  kind="int", force=cfg["name"])
+            assert used == cfg["name"]
+            assert np.array_equal(out.astype(np.float64), ref), (cfg["name"], M, N, K)
+
+
+def test_column_major_swap_identity():
+    """A column-major C = A B is the row-major call with operands swapped."""
+    torch, pk = require_gpu()
+    M, N, K = 96, 80, 40
+    rng = np.random.default_rng(9)
+    A_cm = wl.integers(rng, M * K).reshape(K, M)  # column-major M x K == row-major K x M buffer
+    B_cm = wl.integers(rng, K * N).reshape(N, K)  # column-major K x N
+    dA, dB = dev(A_cm), dev(B_cm)
+    dC = dev(np.zeros((N, M), np.float32))       # column-major M x N
+    st = pk.binding.sgemm("N", "N", N, M, K, 1.0, dB.data_ptr(), K, dA.data_ptr(), M, 0.0, dC.data_ptr(), M)
+    assert st == 0
+    C_cm = host(dC)
+    # the oracle on the same problem stated row-major: A_cm is A^T, B_cm is B^T
+    ref, _ = oracle.sgemm("T", "T", M, N, K, 1.0, A_cm, M, B_cm, K, 0.0, np.zeros((M, N), np.float32), N)
+    assert np.array_equal(C_cm.T.astype(np.float64), ref)
