@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before timing, run one device-to-device copy of this many MiB (a kernel of "
+                         "known traffic that scales the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -154,6 +157,14 @@ def main():
     print("bench: generating inputs", file=sys.stderr, flush=True)
     ops, host = make_ops(torch, pk, wl)
     stream = torch.cuda.current_stream()
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # one untimed pass records which configuration each op runs
     for op in ops:

@@ -132,8 +132,9 @@ const char *pk_status_string(int status);
 /* 1-based argument position of this thread's last PK_ERR_INVALID_VALUE, 0 if none. */
 int pk_last_invalid_param(void);
 
-/* Name of the compiled configuration this thread's last successful call ran
- * ("" for quick returns).  Static storage. */
+/* Name of the compiled configuration this thread's last pk_sgemm or
+ * pk_conv2d_fwd call ran ("" after an error or an empty problem, "scale" for
+ * C <- beta * C).  Static storage. */
 const char *pk_last_config_name(void);
 
 /*

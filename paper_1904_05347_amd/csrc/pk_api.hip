@@ -279,7 +279,7 @@ int pk_num_configs(void)
 
 int pk_get_config(int idx, pk_config_info *info)
 {
-    begin();
+    t_last_param = 0;
     int n = 0;
     const Config *cfgs = pk::configs(&n);
     if (idx < 0 || idx >= n) return invalid(1);
@@ -304,7 +304,7 @@ int pk_get_config(int idx, pk_config_info *info)
 
 int pk_force_config(const char *name)
 {
-    begin();
+    t_last_param = 0;
     if (!name || !*name) {
         t_forced = nullptr;
         t_forced_set = false;
@@ -319,7 +319,7 @@ int pk_force_config(const char *name)
 
 int pk_force_splits(int splits)
 {
-    begin();
+    t_last_param = 0;
     if (splits < 0) return invalid(1);
     t_forced_splits = splits;
     return PK_OK;
