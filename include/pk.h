@@ -152,6 +152,7 @@ typedef struct {
     int vec_a, vec_b; /* elements per global load */
     int stages;      /* LDS buffers (2 = double buffered) */
     int lds_bytes;   /* LDS per work-group */
+    int occupancy;   /* waves per SIMD its registers are allotted for (1 = unconstrained) */
 } pk_config_info;
 
 int pk_num_configs(void);
@@ -173,6 +174,26 @@ int pk_force_config(const char *name);
 /* Forces the split factor of later convolution calls on this thread
  * (0 restores the selector's choice). */
 int pk_force_splits(int splits);
+
+/*
+ * Measurement probes (not part of the operations above): they give the
+ * denominators against which the kernels are judged.
+ *
+ * pk_probe_mfma_peak: `blocks` work-groups of 256 threads, each wave issuing
+ * `iters` x 4 independent v_mfma_f32_32x32x2_f32 (4096 flops each) with no
+ * memory traffic; one float per thread is written to out (blocks * 256
+ * floats, device memory).  Flops = blocks * 4 * iters * 4 * 4096.
+ * pk_probe_mfma_data: the same with operands that differ on every MFMA
+ * (random values read once from src, which holds at least 2^20 floats):
+ * blocks * 4 * iters * 16 MFMAs of 4096 flops.
+ * pk_probe_copy: dst[0:n] = src[0:n] with 16-byte accesses; n a multiple of 4,
+ * both pointers 16-byte aligned device memory.  Bytes moved = 8 * n.
+ * Both are asynchronous on `stream` and return PK_ERR_INVALID_VALUE on bad
+ * arguments (without setting pk_last_invalid_param).
+ */
+int pk_probe_mfma_peak(int blocks, int iters, float *out, void *stream);
+int pk_probe_mfma_data(int blocks, int iters, const float *src, float *out, void *stream);
+int pk_probe_copy(const float *src, float *dst, int64_t n, void *stream);
 
 #ifdef __cplusplus
 }

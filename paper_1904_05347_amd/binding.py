@@ -45,7 +45,7 @@ class ConfigInfo(ctypes.Structure):
                 ("waves_m", ctypes.c_int), ("waves_n", ctypes.c_int), ("threads", ctypes.c_int),
                 ("trans_a", ctypes.c_int), ("trans_b", ctypes.c_int),
                 ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
-                ("stages", ctypes.c_int), ("lds_bytes", ctypes.c_int)]
+                ("stages", ctypes.c_int), ("lds_bytes", ctypes.c_int), ("occupancy", ctypes.c_int)]
 
 
 # Every symbol include/pk.h declares, with its ctypes signature.
@@ -65,6 +65,9 @@ SIGNATURES = {
     "pk_get_config": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ConfigInfo)]),
     "pk_force_config": (ctypes.c_int, [ctypes.c_char_p]),
     "pk_force_splits": (ctypes.c_int, [ctypes.c_int]),
+    "pk_probe_mfma_peak": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, _p, _p]),
+    "pk_probe_mfma_data": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, _p, _p, _p]),
+    "pk_probe_copy": (ctypes.c_int, [_p, _p, _i64, _p]),
 }
 
 
@@ -157,6 +160,55 @@ def force_config(name):
 
 def force_splits(n: int):
     _check(load().pk_force_splits(int(n)), "pk_force_splits")
+
+
+def probe_mfma_peak_tflops(blocks=2048, iters=2000):
+    """Sustained fp32 MFMA rate (TFLOP/s) of back-to-back independent MFMAs."""
+    import torch
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    _check(load().pk_probe_mfma_peak(blocks, iters, out.data_ptr(), s.cuda_stream), "pk_probe_mfma_peak")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    _check(load().pk_probe_mfma_peak(blocks, iters, out.data_ptr(), s.cuda_stream), "pk_probe_mfma_peak")
+    e1.record(s)
+    torch.cuda.synchronize()
+    flops = blocks * 4 * iters * 4 * 4096
+    return flops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+
+
+def probe_mfma_data_tflops(blocks=1024, iters=500):
+    """As probe_mfma_peak_tflops, with random operands that change on every MFMA."""
+    import torch
+    src = torch.rand(1 << 20, dtype=torch.float32, device="cuda") * 2 - 1
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    lib = load()
+    _check(lib.pk_probe_mfma_data(blocks, iters, src.data_ptr(), out.data_ptr(), s.cuda_stream), "probe")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    _check(lib.pk_probe_mfma_data(blocks, iters, src.data_ptr(), out.data_ptr(), s.cuda_stream), "probe")
+    e1.record(s)
+    torch.cuda.synchronize()
+    flops = blocks * 4 * iters * 16 * 4096
+    return flops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+
+
+def probe_copy_gbs(mib=2048, reps=5):
+    """Sustained HBM bandwidth (GB/s, read + write) of a 16-byte streaming copy."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    s = torch.cuda.current_stream()
+    _check(load().pk_probe_copy(src.data_ptr(), dst.data_ptr(), n, s.cuda_stream), "pk_probe_copy")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for _ in range(reps):
+        _check(load().pk_probe_copy(src.data_ptr(), dst.data_ptr(), n, s.cuda_stream), "pk_probe_copy")
+    e1.record(s)
+    torch.cuda.synchronize()
+    return reps * 8 * n / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
 
 # ------------------------------------------------------------ torch tensors

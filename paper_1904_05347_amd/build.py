@@ -22,7 +22,7 @@ CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
     # code object v5: loadable by the HIP runtime that PyTorch ships as well
     "-mcode-object-version=5",
-    "-Wall", "-Wno-unused-result",
+    "-Wall", "-Wno-unused-result", "-Rpass-analysis=kernel-resource-usage",
     # no packed fp32 instructions: hipcc would otherwise form v_pk_* fp32
     # ops from ordinary float code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -25,6 +25,7 @@ struct Config {
     int waves_m, waves_n;
     int trans_a, trans_b;  // GEMM: 1 = operand stored transposed; CONV: always 0
     int vec_a, vec_b;
+    int occupancy;  // waves per SIMD the registers are allotted for (1 = unconstrained)
     int lds_bytes;
     LaunchFn launch;
 };

@@ -1,0 +1,58 @@
+// pk_helpers.hip -- the split-K reduction and the beta-scaling launches.
+#include <hip/hip_runtime.h>
+
+#include "pk_configs.hpp"
+
+namespace pk {
+
+// Fixed-order reduction of split-K partials: C = sum_z ws[z] (+ beta * C).
+// Element e of the M x N result is summed over z = 0, 1, ... in that order,
+// so the result does not depend on scheduling.
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(const float *ws, float *C, int M, int N,
+                                                            int64_t ldc, int splits, float beta)
+{
+    const int64_t total = (int64_t)M * N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
+        float s = ws[e];
+        for (int z = 1; z < splits; ++z) s += ws[e + z * total];
+        const int64_t row = e / N, col = e - row * N;
+        float *c = C + row * ldc + col;
+        *c = beta != 0.f ? fmaf(beta, *c, s) : s;
+    }
+}
+
+// C <- beta * C (alpha == 0 or K == 0).  beta == 0 writes zeros without reading.
+__global__ void __launch_bounds__(256) scale_kernel(float *C, int M, int N, int64_t ldc, float beta)
+{
+    const int64_t total = (int64_t)M * N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
+        const int64_t row = e / N, col = e - row * N;
+        float *c = C + row * ldc + col;
+        *c = beta != 0.f ? beta * *c : 0.f;
+    }
+}
+
+// ---------------------------------------------------------------- helpers
+
+hipError_t launch_splitk_reduce(const float *ws, float *C, int M, int N, int64_t ldc, int splits,
+                                float beta, hipStream_t stream)
+{
+    const int64_t total = (int64_t)M * N;
+    const int64_t blocks = (total + 255) / 256;
+    const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, stream, ws, C, M, N, ldc, splits, beta);
+    return hipGetLastError();
+}
+
+hipError_t launch_scale(float *C, int M, int N, int64_t ldc, float beta, hipStream_t stream)
+{
+    const int64_t total = (int64_t)M * N;
+    const int64_t blocks = (total + 255) / 256;
+    const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);
+    hipLaunchKernelGGL(scale_kernel, dim3(grid), dim3(256), 0, stream, C, M, N, ldc, beta);
+    return hipGetLastError();
+}
+
+}  // namespace pk

@@ -1,0 +1,37 @@
+// pk_instance_common.hpp -- how one tile configuration becomes a kernel
+// instance and a registry entry.  Included by the pk_inst_*.hip files, each of
+// which instantiates one group of configurations (compiled in parallel).
+#pragma once
+
+#include "pk_configs.hpp"
+#include "pk_kernel.hpp"
+
+namespace pk {
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+static hipError_t launch_gemm(const KernelArgs &a, hipStream_t stream)
+{
+    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), 1u, (unsigned)a.splits);
+    const dim3 block(64 * WAVES_M * WAVES_N);
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC>),
+                       grid, block, 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB>
+static constexpr int lds_bytes()
+{
+    return (int)sizeof(float) * GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB>::LDS_FLOATS;
+}
+
+#define PK_GEMM(name, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC)                                         \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC,                                       \
+     lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),                \
+     &launch_gemm<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>}
+
+#define PK_CONV(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                                 \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC,                                         \
+     lds_bytes<BM, BN, BK, WM, WN, A_CONV, false, VA, VB>(),                                          \
+     &launch_gemm<BM, BN, BK, WM, WN, A_CONV, false, VA, VB, OCC>}
+
+
+}  // namespace pk

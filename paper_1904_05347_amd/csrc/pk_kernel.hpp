@@ -288,11 +288,13 @@ struct GemmTile {
     static constexpr int LDS_FLOATS = 2 * (A_STAGE + B_STAGE);
     static constexpr int HALF = BK / 2;
     static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile is made of 32x32 blocks");
-    static_assert(BK % 8 == 0, "BK must be a multiple of 8");
+    static_assert(BK % 16 == 0, "BK must be a multiple of 16 (an even number of 4-step groups per half)");
 };
 
-template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB>
-__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N)
+// OCC: the waves per SIMD the register allocation must leave room for
+// (1 = no constraint beyond the work-group size).
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 gemm_kernel(KernelArgs p)
 {
     typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
@@ -354,7 +356,55 @@ gemm_kernel(KernelArgs p)
     const int a_row = wm * G::WM + l32;
     const int b_row = wn * G::WN + l32;
 
+    // One group = 4 k-steps of the K-block (4 MFMAs per accumulator block).
+    // Operand registers hold two groups: the one being multiplied and the
+    // next one, read from LDS while the current MFMAs run.
+    float fa[2][G::RM][4], fb[2][G::RN][4];
+    auto read_group = [&](const float *as, const float *bs, int g, float (&xa)[G::RM][4],
+                          float (&xb)[G::RN][4]) {
+        const int k0 = h * G::HALF + 4 * g;
+#pragma unroll
+        for (int i = 0; i < G::RM; ++i) {
+            if constexpr (G::A_K) {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(as + (a_row + i * 32) * G::LDA_S + k0);
+                xa[i][0] = v[0]; xa[i][1] = v[1]; xa[i][2] = v[2]; xa[i][3] = v[3];
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) xa[i][t] = as[(k0 + t) * G::LDA_S + a_row + i * 32];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < G::RN; ++j) {
+            if constexpr (B_KCONTIG) {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(bs + (b_row + j * 32) * G::LDB_S + k0);
+                xb[j][0] = v[0]; xb[j][1] = v[1]; xb[j][2] = v[2]; xb[j][3] = v[3];
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) xb[j][t] = bs[(k0 + t) * G::LDB_S + b_row + j * 32];
+            }
+        }
+    };
+    auto mma_group = [&](const float (&xa)[G::RM][4], const float (&xb)[G::RN][4]) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::RN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(xa[i][t], xb[j][t], acc[i][j], 0, 0, 0);
+    };
+
+    // Software pipeline over K-blocks (two LDS stages):
+    //   issue the global loads of block kb+1;
+    //   groups 0..NG-2 of block kb, each overlapping the LDS read of the next group;
+    //   store block kb+1 into the other stage, barrier;
+    //   read group 0 of block kb+1 while the MFMAs of the last group of kb run.
+    // Every read of a stage precedes the barrier that follows it, and every
+    // write of a stage follows the barrier that ends the reads of its previous
+    // contents, so one barrier per K-block orders both.
+    constexpr int NG = G::HALF / 4;
     int stage = 0;
+    if (kbeg < kend) read_group(As, Bs, 0, fa[0], fb[0]);
     for (int kb = kbeg; kb < kend; ++kb) {
         const bool more = kb + 1 < kend;
         if (more) {
@@ -366,45 +416,22 @@ gemm_kernel(KernelArgs p)
         const float *as = As + stage * G::A_STAGE;
         const float *bs = Bs + stage * G::B_STAGE;
 #pragma unroll
-        for (int s4 = 0; s4 < G::HALF; s4 += 4) {
-            float fa[G::RM][4], fb[G::RN][4];
-#pragma unroll
-            for (int i = 0; i < G::RM; ++i) {
-                if constexpr (G::A_K) {
-                    const f32x4 v = *reinterpret_cast<const f32x4 *>(
-                        as + (a_row + i * 32) * G::LDA_S + h * G::HALF + s4);
-                    fa[i][0] = v[0]; fa[i][1] = v[1]; fa[i][2] = v[2]; fa[i][3] = v[3];
-                } else {
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        fa[i][t] = as[(h * G::HALF + s4 + t) * G::LDA_S + a_row + i * 32];
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < G::RN; ++j) {
-                if constexpr (B_KCONTIG) {
-                    const f32x4 v = *reinterpret_cast<const f32x4 *>(
-                        bs + (b_row + j * 32) * G::LDB_S + h * G::HALF + s4);
-                    fb[j][0] = v[0]; fb[j][1] = v[1]; fb[j][2] = v[2]; fb[j][3] = v[3];
-                } else {
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        fb[j][t] = bs[(h * G::HALF + s4 + t) * G::LDB_S + b_row + j * 32];
-                }
-            }
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int i = 0; i < G::RM; ++i)
-#pragma unroll
-                    for (int j = 0; j < G::RN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][t], fb[j][t], acc[i][j], 0, 0, 0);
+        for (int g = 0; g < NG - 1; ++g) {
+            read_group(as, bs, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of these MFMAs
+            mma_group(fa[g & 1], fb[g & 1]);
         }
         if (more) {
             la.template store<G::LDA_S>(As + (stage ^ 1) * G::A_STAGE, ra, tid);
             lb.template store<G::LDB_S>(Bs + (stage ^ 1) * G::B_STAGE, rb, tid);
         }
         __syncthreads();
+        // unconditional (after the last block it reads stale LDS that is never
+        // used): a conditional read would make the compiler copy registers
+        // between the read and the MFMAs below
+        read_group(As + (stage ^ 1) * G::A_STAGE, Bs + (stage ^ 1) * G::B_STAGE, 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_group(fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
         stage ^= 1;
     }
 
@@ -446,35 +473,6 @@ gemm_kernel(KernelArgs p)
                 }
             }
         }
-}
-
-// Fixed-order reduction of split-K partials: C = sum_z ws[z] (+ beta * C).
-// Element e of the M x N result is summed over z = 0, 1, ... in that order,
-// so the result does not depend on scheduling.
-__global__ void __launch_bounds__(256) splitk_reduce_kernel(const float *ws, float *C, int M, int N,
-                                                            int64_t ldc, int splits, float beta)
-{
-    const int64_t total = (int64_t)M * N;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
-        float s = ws[e];
-        for (int z = 1; z < splits; ++z) s += ws[e + z * total];
-        const int64_t row = e / N, col = e - row * N;
-        float *c = C + row * ldc + col;
-        *c = beta != 0.f ? fmaf(beta, *c, s) : s;
-    }
-}
-
-// C <- beta * C (alpha == 0 or K == 0).  beta == 0 writes zeros without reading.
-__global__ void __launch_bounds__(256) scale_kernel(float *C, int M, int N, int64_t ldc, float beta)
-{
-    const int64_t total = (int64_t)M * N;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
-        const int64_t row = e / N, col = e - row * N;
-        float *c = C + row * ldc + col;
-        *c = beta != 0.f ? beta * *c : 0.f;
-    }
 }
 
 }  // namespace pk
