@@ -41,10 +41,49 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
+    ap.add_argument("--probes", action="store_true",
+                    help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
+                         "the HBM copy bandwidth and the vendor fp32 GEMM at 4096^3, print one JSON line")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, run one device-to-device copy of this many MiB (a kernel of "
                          "known traffic that scales the HBM byte counters)")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+
+
+def kernel_source_hash():
+    """Hash of the HIP sources: counters taken on other kernels no longer apply."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1904_05347_amd", "csrc")
+    for path in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        with open(path, "rb") as fh:
+            h.update(os.path.basename(path).encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(op_name, config):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary, scaled by the copy-kernel calibration; None when that summary was
+    taken on different kernel sources or lacks this launch."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            lines = fh.read().splitlines()
+    except OSError:
+        return None
+    fields = dict(l.split(None, 1) for l in lines if l.startswith("source_hash "))
+    if fields.get("source_hash", "").strip() != kernel_source_hash():
+        return None
+    for l in lines:
+        if l.startswith("traffic |"):
+            parts = [x.strip() for x in l.split("|")]
+            if parts[1] == op_name and parts[2] == config:
+                return int(parts[5])
+    return None
 
 
 class Op:
@@ -137,6 +176,35 @@ def cpu_baseline(oracle, host, ops, seconds, np):
     }
 
 
+def run_probes(torch, pk):
+    """Denominators measured on this GPU, and the vendor fp32 GEMM as context."""
+    from paper_1904_05347_amd import binding
+    warm = torch.rand(4096, 4096, device="cuda")
+    for _ in range(40):
+        pk.gemm(warm, warm)
+    torch.cuda.synchronize()
+    out = {"mfma_const_operands_tflops": {}, "mfma_random_operands_tflops": {}}
+    for blocks in (768, 2048):  # 768 = one round of 3 work-groups per CU
+        out["mfma_const_operands_tflops"][blocks] = round(binding.probe_mfma_peak_tflops(blocks, 8000), 2)
+        out["mfma_random_operands_tflops"][blocks] = round(binding.probe_mfma_data_tflops(blocks, 2000), 2)
+    out["copy_gbs_2GiB"] = round(binding.probe_copy_gbs(2048), 1)
+    torch.backends.cuda.matmul.allow_tf32 = False
+    a = torch.rand(4096, 4096, device="cuda") * 2 - 1
+    b = torch.rand(4096, 4096, device="cuda") * 2 - 1
+    for _ in range(3):
+        a @ b
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 10
+    out["vendor_fp32_gemm_4096_tflops"] = round(2 * 4096 ** 3 / (ms * 1e-3) / 1e12, 2)
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -154,6 +222,9 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     pk.load()
+    if args.probes:
+        print(json.dumps(run_probes(torch, pk)))
+        return
     print("bench: generating inputs", file=sys.stderr, flush=True)
     ops, host = make_ops(torch, pk, wl)
     stream = torch.cuda.current_stream()
@@ -203,7 +274,8 @@ def main():
     dom = max(range(len(ops)), key=lambda i: per_op[i]["ms"])
     d = per_op[dom]
     roofline = {"bound": "mfma", "achieved": d["tflops"], "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(d["tflops"] / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                "frac": round(d["tflops"] / FP32_MFMA_PEAK_TFLOPS, 4),
+                "traffic": measured_traffic(d["op"], d["config"]),
                 "kernel": d["config"], "workload": d["op"], "avg_launch_ms": d["ms"],
                 "flops_per_launch": ops[dom].flops}
 

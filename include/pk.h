@@ -144,7 +144,7 @@ const char *pk_last_config_name(void);
  */
 typedef struct {
     const char *name;
-    int kind;        /* 0 = GEMM, 1 = implicit-GEMM convolution */
+    int kind;        /* 0 = GEMM, 1 = implicit-GEMM convolution, 2 = tiled direct convolution */
     int bm, bn, bk;  /* work-group tile and K-block depth */
     int waves_m, waves_n; /* wave grid; each wave owns (bm/waves_m) x (bn/waves_n) */
     int threads;     /* work-group size */

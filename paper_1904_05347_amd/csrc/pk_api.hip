@@ -165,6 +165,7 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, bool 
 
 bool conv_config_fits(const Config *c, bool va4, bool vb4)
 {
+    if (c->kind == pk::KIND_DIRECT) return true;  // checked against the window by the caller
     if (c->kind != pk::KIND_CONV) return false;
     if (c->vec_a > 1 && !va4) return false;
     if (c->vec_b > 1 && !vb4) return false;
@@ -437,6 +438,7 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
     if (M < 0 || K < 0 || M > kMaxDim || K > kMaxDim || Cout > kMaxDim) return 0;
     // the selector's choice for 16-byte aligned tensors (what the allocator gives)
     const bool v4 = Cin % 4 == 0 && Cout % 4 == 0;
+    if (!gemm_path && pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535) return 0;
     const Config *c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
     if (!c) return 0;
     const int splits = t_forced_splits > 0 ? t_forced_splits : choose_splits(c, M, Cout, K);
@@ -518,12 +520,16 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     } else {
         const bool va4 = Cin % 4 == 0 && aligned16(x);
         const bool vb4 = Cout % 4 == 0 && aligned16(f);
+        const bool direct_ok = pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535;
         if (c) {
             if (!conv_config_fits(c, va4, vb4)) return PK_ERR_NOT_SUPPORTED;
+            if (c->kind == pk::KIND_DIRECT && !direct_ok) return PK_ERR_NOT_SUPPORTED;
+        } else if (direct_ok) {
+            c = find_config("direct_8x32x64_k32");
         } else {
             c = select_conv(M, Cout, va4, vb4);
-            if (!c) return PK_ERR_NOT_SUPPORTED;
         }
+        if (!c) return PK_ERR_NOT_SUPPORTED;
         a.H = (int)H;
         a.W = (int)W;
         a.Cin = (int)Cin;
@@ -534,6 +540,18 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         a.pl = (int)pl;
         a.Ho = (int)Ho;
         a.Wo = (int)Wo;
+        a.KH = (int)KH;
+        a.batch = (int)N;
+    }
+    if (c->kind == pk::KIND_DIRECT) {
+        a.A = x;
+        a.M = (int)M;
+        a.N = (int)Cout;
+        a.K = (int)K;
+        a.splits = 1;
+        if (c->launch(a, s) != hipSuccess) return PK_ERR_LAUNCH;
+        t_last_config = c->name;
+        return PK_OK;
     }
     int splits = 1;
     const size_t per_split = (size_t)M * (size_t)Cout * sizeof(float);

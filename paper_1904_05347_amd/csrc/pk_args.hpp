@@ -19,6 +19,7 @@ struct KernelArgs {
     // implicit-GEMM geometry: A(m, k) = x[n][ho*sh - pt + kh][wo*sw - pl + kw][ci]
     // with m = (n*Ho + ho)*Wo + wo and k = (kh*KW + kw)*Cin + ci.
     int H, W, Cin, KW, sh, sw, pt, pl, Ho, Wo;
+    int KH, batch;  // used by the direct convolution only
 };
 
 }  // namespace pk

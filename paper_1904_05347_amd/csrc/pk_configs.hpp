@@ -14,7 +14,7 @@
 
 namespace pk {
 
-enum Kind { KIND_GEMM = 0, KIND_CONV = 1 };
+enum Kind { KIND_GEMM = 0, KIND_CONV = 1, KIND_DIRECT = 2 };
 
 typedef hipError_t (*LaunchFn)(const KernelArgs &args, hipStream_t stream);
 
@@ -35,6 +35,10 @@ const Config *configs(int *count);
 
 hipError_t launch_splitk_reduce(const float *ws, float *C, int M, int N, int64_t ldc, int splits,
                                 float beta, hipStream_t stream);
+// Whether the tiled direct convolution takes this window (short reduction,
+// input patch fits its LDS buffer).
+bool direct_conv_fits(int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t sw);
+
 hipError_t launch_scale(float *C, int M, int N, int64_t ldc, float beta, hipStream_t stream);
 
 }  // namespace pk

@@ -123,6 +123,9 @@ def test_config_space(pk):
     assert len(set(names)) == len(names)
     for c in cfgs:
         assert c["threads"] == 64 * c["waves_m"] * c["waves_n"]
+        assert c["lds_bytes"] <= 160 * 1024
+        if c["kind"] == 2:  # tiled direct convolution: one LDS input patch
+            continue
         assert c["bm"] % (32 * c["waves_m"]) == 0 and c["bn"] % (32 * c["waves_n"]) == 0
         assert c["bk"] % 8 == 0
         assert c["stages"] == 2

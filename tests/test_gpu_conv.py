@@ -81,12 +81,48 @@ def test_every_conv_config_forced():
     x = wl.integers(rng, 2 * 11 * 10 * 8).reshape(2, 11, 10, 8)
     f = wl.integers(rng, 3 * 3 * 8 * 20).reshape(3, 3, 8, 20)
     ref, _ = oracle.conv2d(x, f, (1, 1), (1, 1, 1, 1))
+    # a window the direct kernel takes (KH*KW*Cin <= 32)
+    xs = wl.integers(rng, 2 * 11 * 10 * 3).reshape(2, 11, 10, 3)
+    fs = wl.integers(rng, 3 * 3 * 3 * 20).reshape(3, 3, 3, 20)
+    ref_s, _ = oracle.conv2d(xs, fs, (1, 1), (1, 1, 1, 1))
     for cfg in pk.configs():
-        if cfg["kind"] != 1:
-            continue
-        out, used = _run(pk, x, f, (1, 1), (1, 1, 1, 1), force=cfg["name"])
-        assert used == cfg["name"]
-        assert np.array_equal(out.astype(np.float64), ref), cfg["name"]
+        if cfg["kind"] == 1:
+            out, used = _run(pk, x, f, (1, 1), (1, 1, 1, 1), force=cfg["name"])
+            assert used == cfg["name"]
+            assert np.array_equal(out.astype(np.float64), ref), cfg["name"]
+        if cfg["kind"] in (1, 2) and cfg["vec_a"] == 1:
+            out, used = _run(pk, xs, fs, (1, 1), (1, 1, 1, 1), force=cfg["name"])
+            assert used == cfg["name"]
+            assert np.array_equal(out.astype(np.float64), ref_s), cfg["name"]
+
+
+DIRECT_GEOMS = [
+    # (N, H, W, Cin, KH, KW, Cout, stride, pads): ragged tiles, channel groups, strides
+    (3, 13, 45, 3, 3, 3, 100, (1, 1), (1, 1, 1, 1)),
+    (2, 17, 70, 3, 3, 3, 64, (2, 2), (0, 0, 1, 1)),
+    (1, 9, 33, 1, 5, 5, 7, (1, 1), (2, 2, 2, 2)),
+    (2, 8, 31, 4, 2, 4, 130, (2, 1), (1, 0, 0, 3)),
+    (1, 40, 40, 2, 4, 4, 32, (3, 3), (0, 0, 0, 0)),
+]
+
+
+@pytest.mark.parametrize("geom", DIRECT_GEOMS, ids=lambda g: "x".join(map(str, g[:7])) + "_s%d%d" % g[7])
+def test_direct_conv_geometries(geom):
+    torch, pk = require_gpu()
+    N, H, W, Cin, KH, KW, Cout, stride, pads = geom
+    rng = np.random.default_rng(sum(geom[:7]) + 1)
+    x = wl.uniform(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+    f = wl.uniform(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
+    out, cfg = _run(pk, x, f, stride, pads)
+    assert cfg.startswith("direct"), cfg
+    ref, scale = oracle.conv2d(x, f, stride, pads)
+    assert out.shape == ref.shape
+    assert_parity(out, ref, scale, str(geom) + " " + cfg)
+    xi = wl.integers(rng, x.size).reshape(x.shape)
+    fi = wl.integers(rng, f.size).reshape(f.shape)
+    out, cfg = _run(pk, xi, fi, stride, pads)
+    ref, _ = oracle.conv2d(xi, fi, stride, pads)
+    assert np.array_equal(out.astype(np.float64), ref), (geom, cfg)
 
 
 @pytest.mark.parametrize("splits", [2, 3, 5])
