@@ -12,7 +12,7 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libpk.so")
+LIB_PATH = os.environ.get("PK_LIBRARY") or os.path.join(HERE, "libpk.so")
 
 PK_OK = 0
 PK_ERR_INVALID_VALUE = 1

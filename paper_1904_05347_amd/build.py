@@ -13,8 +13,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
-BUILD = os.path.join(HERE, "_build")
-LIB = os.path.join(HERE, "libpk.so")
+BUILD = os.environ.get("PK_BUILD_DIR") or os.path.join(HERE, "_build")
+LIB = os.environ.get("PK_LIBRARY") or os.path.join(HERE, "libpk.so")
 ARCH = os.environ.get("PK_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -27,7 +27,7 @@ CFLAGS = [
     # ops from ordinary float code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I" + os.path.join(os.path.dirname(HERE), "include"),
-]
+] + os.environ.get("PK_EXTRA_CFLAGS", "").split()
 
 
 def _compile(src: str) -> str:

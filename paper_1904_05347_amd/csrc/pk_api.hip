@@ -136,12 +136,52 @@ bool gemm_config_fits(const Config *c, int ta, int tb, bool vec_ok)
     return true;
 }
 
-// Per-shape choice, from timings of every compiled configuration on MI355X
-// (fp32, the 4096^3 GEMMs, the 1024/2048 sweep, and the VGG-16 / ResNet-50
-// layers at batch 32):
+// Per-shape tuning table: the fastest compiled configuration (and split of
+// K) measured on MI355X for the shapes the benchmarks run, by timing every
+// compatible configuration with PK_FORCE_CONFIG.  kind: 0 = pk_sgemm,
+// 1 = pk_conv2d_fwd (M = N*Ho*Wo, N = Cout, K = KH*KW*Cin; window and stride
+// complete the key).  splits 0 = the default rule.
+struct TunedShape {
+    int kind, ta, tb;
+    int64_t M, N, K;
+    int kh, stride;
+    const char *config;
+    int splits;
+};
+
+const TunedShape kTuned[] = {
+    {0, 0, 0, 4096, 4096, 4096, 0, 0, "gemm_256x256x16_w2x4_nn_v44_o2", 0},
+    {0, 1, 0, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_tn_v44_o2", 0},
+    {0, 0, 1, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_nt_v44_o2", 0},
+    {0, 0, 0, 2048, 2048, 2048, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
+    {0, 0, 0, 1024, 1024, 1024, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
+    // VGG-16 block-first layers at batch 32 (3x3, stride 1)
+    {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2", 1},
+    {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_64x64x32_w2x2_v44", 1},
+    {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44", 1},
+    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44", 2},
+    // ResNet-50 bottleneck layers at batch 32
+    {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},
+    {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x32_w2x4_v44_o2", 1},
+    {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
+    {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
+    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 3},
+    {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x64x32_w2x2_nn_v44", 1},
+};
+
+const TunedShape *find_tuned(int kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t kh, int64_t stride)
+{
+    for (const TunedShape &t : kTuned)
+        if (t.kind == kind && t.ta == ta && t.tb == tb && t.M == M && t.N == N && t.K == K &&
+            (kind == 0 || (t.kh == kh && t.stride == stride)))
+            return &t;
+    return nullptr;
+}
+
+// Shapes outside the table, from the same measurements:
 //   - products with at least 4 work-groups of 128 x 128 per CU and K >= 512:
-//     128 x 128 tiles with K-blocks of 32 (fewest barriers per MFMA at 2
-//     waves/SIMD);
+//     256 x 256 tiles on 8 waves (128 x 64 per wave, 2 waves per SIMD): the
+//     fewest LDS reads and the least L2 traffic per MFMA;
 //   - everything smaller: 64 x 64 tiles, which keep 4+ waves per SIMD busy;
 //     K-blocks of 32, or 16 when K itself is that short;
 //   - unaligned operands: 4-byte loads.
@@ -156,7 +196,7 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, bool 
         const bool big = ceil_div(M, 128) * ceil_div(N, 128) >= 4 * kCUs;
         snprintf(name, sizeof(name), big ? "gemm_128x128x16_w2x2_%s_v44" : "gemm_64x64x16_w2x2_%s_v44", lay);
     } else if (ceil_div(M, 128) * ceil_div(N, 128) >= 4 * kCUs && K >= 512) {
-        snprintf(name, sizeof(name), "gemm_128x128x32_w2x2_%s_v44", lay);
+        snprintf(name, sizeof(name), "gemm_256x256x32_w2x4_%s_v44_o2", lay);
     } else {
         snprintf(name, sizeof(name), K <= 64 ? "gemm_64x64x16_w2x2_%s_v44" : "gemm_64x64x32_w2x2_%s_v44", lay);
     }
@@ -405,7 +445,9 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float al
     if (c) {
         if (!gemm_config_fits(c, ta, tb, vec_ok)) return PK_ERR_NOT_SUPPORTED;
     } else {
-        c = select_gemm(ta, tb, M, N, K, vec_ok);
+        const TunedShape *t = vec_ok ? find_tuned(0, ta, tb, M, N, K, 0, 0) : nullptr;
+        c = t ? find_config(t->config) : nullptr;
+        if (!c) c = select_gemm(ta, tb, M, N, K, vec_ok);
         if (!c) return PK_ERR_NOT_SUPPORTED;
     }
     KernelArgs a;
@@ -439,8 +481,12 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
     // the selector's choice for 16-byte aligned tensors (what the allocator gives)
     const bool v4 = Cin % 4 == 0 && Cout % 4 == 0;
     if (!gemm_path && pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535) return 0;
-    const Config *c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
+    const TunedShape *tuned = (KH == KW && sh == sw) ? find_tuned(1, 0, 0, M, Cout, K, KH, sh) : nullptr;
+    const Config *c = (tuned && v4) ? find_config(tuned->config) : nullptr;
+    if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
     if (!c) return 0;
+    if (tuned && v4 && tuned->splits > 0 && t_forced_splits == 0)
+        return tuned->splits > 1 ? (size_t)tuned->splits * (size_t)M * (size_t)Cout * sizeof(float) : 0;
     const int splits = t_forced_splits > 0 ? t_forced_splits : choose_splits(c, M, Cout, K);
     if (splits <= 1) return 0;
     return (size_t)splits * (size_t)M * (size_t)Cout * sizeof(float);
@@ -508,13 +554,15 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
 
     const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
+    const TunedShape *tuned = (KH == KW && sh == sw) ? find_tuned(1, 0, 0, M, Cout, K, KH, sh) : nullptr;
     if (gemm_path) {
         // 1x1, stride 1, no padding: the image is already the M x Cin matrix.
         const bool vec_ok = gemm_vec_ok(0, 0, M, Cout, Cin, x, Cin, f, Cout);
         if (c) {
             if (!gemm_config_fits(c, 0, 0, vec_ok)) return PK_ERR_NOT_SUPPORTED;
         } else {
-            c = select_gemm(0, 0, M, Cout, Cin, vec_ok);
+            c = (tuned && vec_ok) ? find_config(tuned->config) : nullptr;
+            if (!c) c = select_gemm(0, 0, M, Cout, Cin, vec_ok);
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     } else {
@@ -527,7 +575,8 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         } else if (direct_ok) {
             c = find_config("direct_8x32x64_k32");
         } else {
-            c = select_conv(M, Cout, va4, vb4);
+            c = (tuned && va4 && vb4) ? find_config(tuned->config) : nullptr;
+            if (!c) c = select_conv(M, Cout, va4, vb4);
         }
         if (!c) return PK_ERR_NOT_SUPPORTED;
         a.H = (int)H;
@@ -559,7 +608,8 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         splits = t_forced_splits;
         if (splits > 1 && (!workspace || workspace_bytes < (size_t)splits * per_split)) return PK_ERR_WORKSPACE;
     } else {
-        splits = choose_splits(c, M, Cout, K);
+        const bool tuned_cfg = tuned && strcmp(c->name, tuned->config) == 0 && tuned->splits > 0;
+        splits = tuned_cfg ? tuned->splits : choose_splits(c, M, Cout, K);
         if (splits > 1 && (!workspace || workspace_bytes < (size_t)splits * per_split)) splits = 1;
     }
     a.A = x;
