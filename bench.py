@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
+    ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep"),
+                    help="step: the benchmark step (default); layers: every VGG-16 / ResNet-50 layer of the "
+                         "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
+                         "the vendor fp32 GEMM beside it")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
                          "the HBM copy bandwidth and the vendor fp32 GEMM at 4096^3, print one JSON line")
@@ -176,6 +180,77 @@ def cpu_baseline(oracle, host, ops, seconds, np):
     }
 
 
+def _time_ms(torch, fn, min_ms=20.0):
+    """Mean duration of fn on the current stream: 2 warm-up calls, then enough
+    calls to span about min_ms."""
+    fn()
+    fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    fn()
+    e1.record()
+    torch.cuda.synchronize()
+    one = max(e0.elapsed_time(e1), 1e-3)
+    iters = int(min(max(min_ms / one, 3), 200))
+    e0.record()
+    for _ in range(iters):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / iters
+
+
+def run_layer_suite(torch, pk, wl):
+    """Every distinct layer of the paper's VGG-16 / ResNet-50 tables at batch 1, 4, 32."""
+    rows = []
+    for batch in (1, 4, 32):
+        for case in wl.layer_suite(batch):
+            x, f = case.inputs()
+            N, H, W, Cin = case.x_shape
+            KH, KW, _, Cout = case.f_shape
+            Ho, Wo = pk.conv2d_out_dims(H, W, KH, KW, *case.stride, *case.pads)
+            dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+            dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+            wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
+            ws = torch.empty(wsb // 4, dtype=torch.float32, device="cuda") if wsb else None
+
+            def run():
+                pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads, out=dy, workspace=ws)
+
+            ms = _time_ms(torch, run)
+            flops = wl.conv_flops(case, Ho, Wo)
+            nbytes = 4 * (x.size + f.size + N * Ho * Wo * Cout)
+            rows.append({"layer": case.name, "config": pk.last_config_name(), "ms": round(ms, 4),
+                         "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+                         "frac_mfma_peak": round(flops / (ms * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4),
+                         "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                         "flop_per_byte": round(flops / nbytes, 1)})
+            del dx, df, dy, ws
+            print("bench: %s %.4f ms" % (case.name, ms), file=sys.stderr, flush=True)
+    return {"suite": "layers", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
+def run_gemm_sweep(torch, pk, wl):
+    """The paper's GEMM sweep (M, N, K powers of two in [64, 1024]), with the
+    vendor fp32 GEMM (torch.matmul, tf32 off) timed beside it as context."""
+    torch.backends.cuda.matmul.allow_tf32 = False
+    rows = []
+    for case in wl.gemm_sweep():
+        A, B, C = case.inputs()
+        dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+        dC = torch.empty((case.M, case.N), dtype=torch.float32, device="cuda")
+        ms = _time_ms(torch, lambda: pk.gemm(dA, dB, dC))
+        cfg = pk.last_config_name()
+        ms_v = _time_ms(torch, lambda: torch.matmul(dA, dB, out=dC))
+        nbytes = 4 * (case.M * case.K + case.K * case.N + case.M * case.N)
+        rows.append({"M": case.M, "N": case.N, "K": case.K, "config": cfg,
+                     "flop_per_byte": round(case.flops / nbytes, 2),
+                     "gflops": round(case.flops / (ms * 1e-3) / 1e9, 1),
+                     "vendor_gflops": round(case.flops / (ms_v * 1e-3) / 1e9, 1)})
+    return {"suite": "gemm-sweep", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
 def run_probes(torch, pk):
     """Denominators measured on this GPU, and the vendor fp32 GEMM as context."""
     from paper_1904_05347_amd import binding
@@ -224,6 +299,12 @@ def main():
     pk.load()
     if args.probes:
         print(json.dumps(run_probes(torch, pk)))
+        return
+    if args.suite == "layers":
+        print(json.dumps(run_layer_suite(torch, pk, wl)))
+        return
+    if args.suite == "gemm-sweep":
+        print(json.dumps(run_gemm_sweep(torch, pk, wl)))
         return
     print("bench: generating inputs", file=sys.stderr, flush=True)
     ops, host = make_ops(torch, pk, wl)

@@ -153,6 +153,7 @@ typedef struct {
     int stages;      /* LDS buffers (2 = double buffered) */
     int lds_bytes;   /* LDS per work-group */
     int occupancy;   /* waves per SIMD its registers are allotted for (1 = unconstrained) */
+    int persistent;  /* 1 = one work-group per resident slot, each looping over tiles */
 } pk_config_info;
 
 int pk_num_configs(void);

@@ -45,7 +45,8 @@ class ConfigInfo(ctypes.Structure):
                 ("waves_m", ctypes.c_int), ("waves_n", ctypes.c_int), ("threads", ctypes.c_int),
                 ("trans_a", ctypes.c_int), ("trans_b", ctypes.c_int),
                 ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
-                ("stages", ctypes.c_int), ("lds_bytes", ctypes.c_int), ("occupancy", ctypes.c_int)]
+                ("stages", ctypes.c_int), ("lds_bytes", ctypes.c_int), ("occupancy", ctypes.c_int),
+                ("persistent", ctypes.c_int)]
 
 
 # Every symbol include/pk.h declares, with its ctypes signature.

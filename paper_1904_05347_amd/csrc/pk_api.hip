@@ -347,6 +347,7 @@ int pk_get_config(int idx, pk_config_info *info)
     info->stages = 2;
     info->lds_bytes = c->lds_bytes;
     info->occupancy = c->occupancy;
+    info->persistent = c->persistent;
     return PK_OK;
 }
 

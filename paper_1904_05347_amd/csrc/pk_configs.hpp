@@ -26,6 +26,7 @@ struct Config {
     int trans_a, trans_b;  // GEMM: 1 = operand stored transposed; CONV: always 0
     int vec_a, vec_b;
     int occupancy;  // waves per SIMD the registers are allotted for (1 = unconstrained)
+    int persistent; // 1 = grid sized to the resident work-groups, each looping over tiles
     int lds_bytes;
     LaunchFn launch;
 };
@@ -35,6 +36,9 @@ const Config *configs(int *count);
 
 hipError_t launch_splitk_reduce(const float *ws, float *C, int M, int N, int64_t ldc, int splits,
                                 float beta, hipStream_t stream);
+// Compute units of the current device (queried once per device).
+int device_cu_count();
+
 // Whether the tiled direct convolution takes this window (short reduction,
 // input patch fits its LDS buffer).
 bool direct_conv_fits(int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t sw);

@@ -154,7 +154,7 @@ bool direct_conv_fits(int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t s
 const Config *configs_direct(int *count)
 {
     static const Config kTable[] = {
-        {"direct_8x32x64_k32", KIND_DIRECT, DT_ROWS * DT_COLS, DT_CH, DT_KMAX, DT_WAVES, 1, 0, 0, 1, 1, 1,
+        {"direct_8x32x64_k32", KIND_DIRECT, DT_ROWS * DT_COLS, DT_CH, DT_KMAX, DT_WAVES, 1, 0, 0, 1, 1, 1, 0,
          (int)(DT_LDS_FLOATS * sizeof(float)), &launch_direct},
     };
     *count = (int)(sizeof(kTable) / sizeof(kTable[0]));

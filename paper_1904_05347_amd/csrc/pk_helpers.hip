@@ -36,6 +36,19 @@ __global__ void __launch_bounds__(256) scale_kernel(float *C, int M, int N, int6
 
 // ---------------------------------------------------------------- helpers
 
+int device_cu_count()
+{
+    static int counts[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+    if (counts[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
+        counts[dev] = n;
+    }
+    return counts[dev];
+}
+
 hipError_t launch_splitk_reduce(const float *ws, float *C, int M, int N, int64_t ldc, int splits,
                                 float beta, hipStream_t stream)
 {

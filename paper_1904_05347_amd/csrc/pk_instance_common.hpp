@@ -17,6 +17,27 @@ static hipError_t launch_gemm(const KernelArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
+// Persistent launch: as many work-groups as the CUs hold at once (from the
+// occupancy the compiled kernel allows), each walking its share of the tiles.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+static hipError_t launch_gemm_persistent(const KernelArgs &a, hipStream_t stream)
+{
+    auto kernel = gemm_persistent_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC>;
+    const int threads = 64 * WAVES_M * WAVES_N;
+    static int per_cu = 0;  // resident work-groups per CU (same on every MI355X)
+    if (per_cu == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
+        per_cu = n;
+    }
+    const int64_t items = (int64_t)a.tiles_m * a.tiles_n * a.splits;
+    int64_t grid = (int64_t)per_cu * device_cu_count();
+    if (grid > items) grid = items;
+    if (grid >= a.xcds && a.xcds > 1) grid -= grid % a.xcds;
+    hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(threads), 0, stream, a);
+    return hipGetLastError();
+}
+
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB>
 static constexpr int lds_bytes()
 {
@@ -24,14 +45,24 @@ static constexpr int lds_bytes()
 }
 
 #define PK_GEMM(name, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC)                                         \
-    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC,                                       \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC, 0,                                    \
      lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),                \
      &launch_gemm<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>}
 
 #define PK_CONV(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                                 \
-    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC,                                         \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 0,                                      \
      lds_bytes<BM, BN, BK, WM, WN, A_CONV, false, VA, VB>(),                                          \
      &launch_gemm<BM, BN, BK, WM, WN, A_CONV, false, VA, VB, OCC>}
+
+#define PK_GEMM_P(name, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC)                                       \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC, 1,                                    \
+     lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),                \
+     &launch_gemm_persistent<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>}
+
+#define PK_CONV_P(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                               \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 1,                                      \
+     lds_bytes<BM, BN, BK, WM, WN, A_CONV, false, VA, VB>(),                                          \
+     &launch_gemm_persistent<BM, BN, BK, WM, WN, A_CONV, false, VA, VB, OCC>}
 
 
 }  // namespace pk

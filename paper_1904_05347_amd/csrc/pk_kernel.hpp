@@ -45,6 +45,18 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 enum AMode { A_KCONTIG = 0, A_MCONTIG = 1, A_CONV = 2 };
 
 
+// Tile (tm, tn) of logical tile index t, in column strips of group_m tile-rows.
+__device__ __forceinline__ void tile_of(const KernelArgs &p, int t, int &tm, int &tn)
+{
+    const int group = p.group_m * p.tiles_n;
+    const int gid = t / group;
+    const int first_m = gid * p.group_m;
+    const int gsz = min(p.tiles_m - first_m, p.group_m);
+    const int in_group = t - gid * group;
+    tm = first_m + in_group % gsz;
+    tn = in_group / gsz;
+}
+
 // Maps the linear work-group id to a C tile.  Work-groups are handed to the
 // 8 XCDs round-robin (id % 8); renumbering them so that each XCD receives a
 // contiguous run of logical tiles keeps the A and B panels those tiles share
@@ -59,13 +71,7 @@ __device__ __forceinline__ void tile_coords(const KernelArgs &p, int &tm, int &t
         const int x = pid % p.xcds, loc = pid / p.xcds;
         pid = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + loc;
     }
-    const int group = p.group_m * p.tiles_n;
-    const int gid = pid / group;
-    const int first_m = gid * p.group_m;
-    const int gsz = min(p.tiles_m - first_m, p.group_m);
-    const int in_group = pid - gid * group;
-    tm = first_m + in_group % gsz;
-    tn = in_group / gsz;
+    tile_of(p, pid, tm, tn);
 }
 
 template <int V>
@@ -281,15 +287,124 @@ struct GemmTile {
     static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     static constexpr int RM = WM / 32, RN = WN / 32;
     static constexpr bool A_K = AMODE != A_MCONTIG;  // A staged k-contiguous
+    static constexpr bool B_K = B_KCONTIG;           // B staged k-contiguous
     static constexpr int LDA_S = A_K ? BK + LDS_PAD : BM + LDS_PAD;
     static constexpr int LDB_S = B_KCONTIG ? BK + LDS_PAD : BN + LDS_PAD;
     static constexpr int A_STAGE = A_K ? BM * LDA_S : BK * LDA_S;
     static constexpr int B_STAGE = B_KCONTIG ? BN * LDB_S : BK * LDB_S;
     static constexpr int LDS_FLOATS = 2 * (A_STAGE + B_STAGE);
     static constexpr int HALF = BK / 2;
+    static constexpr int NG = HALF / 4;  // 4-step groups per K-block
     static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile is made of 32x32 blocks");
     static_assert(BK % 16 == 0, "BK must be a multiple of 16 (an even number of 4-step groups per half)");
+
+    typedef typename ALoaderSel<AMODE, BM, BK, VA, NT>::T ALoader;
+    typedef typename std::conditional<B_KCONTIG, KContigLoader<BN, BK, VB, NT>,
+                                      MContigLoader<BN, BK, VB, NT>>::type BLoader;
+    typedef f32x16 Acc[RM][RN];
+    typedef float FragA[RM][4];
+    typedef float FragB[RN][4];
+
+    // Operands of one group (4 k-steps) for this lane, from one LDS stage.
+    // a_row / b_row: the lane's row of the wave's first 32-row (-column) block.
+    static __device__ __forceinline__ void read_group(const float *as, const float *bs, int a_row, int b_row,
+                                                      int h, int g, FragA &xa, FragB &xb)
+    {
+        const int k0 = h * HALF + 4 * g;
+#pragma unroll
+        for (int i = 0; i < RM; ++i) {
+            if constexpr (A_K) {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(as + (a_row + i * 32) * LDA_S + k0);
+                xa[i][0] = v[0]; xa[i][1] = v[1]; xa[i][2] = v[2]; xa[i][3] = v[3];
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) xa[i][t] = as[(k0 + t) * LDA_S + a_row + i * 32];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < RN; ++j) {
+            if constexpr (B_K) {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(bs + (b_row + j * 32) * LDB_S + k0);
+                xb[j][0] = v[0]; xb[j][1] = v[1]; xb[j][2] = v[2]; xb[j][3] = v[3];
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) xb[j][t] = bs[(k0 + t) * LDB_S + b_row + j * 32];
+            }
+        }
+    }
+
+    static __device__ __forceinline__ void mma_group(Acc &acc, const FragA &xa, const FragB &xb)
+    {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int i = 0; i < RM; ++i)
+#pragma unroll
+                for (int j = 0; j < RN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(xa[i][t], xb[j][t], acc[i][j], 0, 0, 0);
+    }
+
+    static __device__ __forceinline__ void zero(Acc &acc)
+    {
+#pragma unroll
+        for (int i = 0; i < RM; ++i)
+#pragma unroll
+            for (int j = 0; j < RN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    }
+
+    // Epilogue of one tile: C = alpha * acc (+ beta * C), or split z's partial
+    // sum alpha * acc into the workspace.  Lane (l32, h) of the wave holds
+    // C(row_base + i*32 + 8*(r/4) + r%4, col_base + j*32) in acc[i][j][r].
+    static __device__ __forceinline__ void store(const KernelArgs &p, const Acc &acc, int row_base, int col_base,
+                                                 int z)
+    {
+        if (p.splits > 1) {
+            float *out = p.ws + (int64_t)z * p.M * p.N;
+#pragma unroll
+            for (int i = 0; i < RM; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                    if (row < p.M) {
+#pragma unroll
+                        for (int j = 0; j < RN; ++j) {
+                            const int col = col_base + j * 32;
+                            if (col < p.N) out[(int64_t)row * p.N + col] = p.alpha * acc[i][j][r];
+                        }
+                    }
+                }
+            return;
+        }
+#pragma unroll
+        for (int i = 0; i < RM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                if (row < p.M) {
+                    float *crow = p.C + (int64_t)row * p.ldc;
+#pragma unroll
+                    for (int j = 0; j < RN; ++j) {
+                        const int col = col_base + j * 32;
+                        if (col < p.N) {
+                            float v = p.alpha * acc[i][j][r];
+                            if (p.beta != 0.f) v = fmaf(p.beta, crow[col], v);
+                            crow[col] = v;
+                        }
+                    }
+                }
+            }
+    }
 };
+
+// K range [kbeg, kend) of split z.
+__device__ __forceinline__ void split_range(const KernelArgs &p, int bk, int z, int &kbeg, int &kend)
+{
+    const int nkb = (p.K + bk - 1) / bk;
+    kbeg = z * p.kblocks_per_split;
+    kend = min(nkb, kbeg + p.kblocks_per_split);
+}
 
 // OCC: the waves per SIMD the register allocation must leave room for
 // (1 = no constraint beyond the work-group size).
@@ -298,10 +413,8 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_
 gemm_kernel(KernelArgs p)
 {
     typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
-    constexpr int NT = G::NT;
-    typedef typename ALoaderSel<AMODE, BM, BK, VA, NT>::T ALoader;
-    typedef typename std::conditional<B_KCONTIG, KContigLoader<BN, BK, VB, NT>,
-                                      MContigLoader<BN, BK, VB, NT>>::type BLoader;
+    typedef typename G::ALoader ALoader;
+    typedef typename G::BLoader BLoader;
 
     __shared__ __attribute__((aligned(16))) float smem[G::LDS_FLOATS];
     float *As = smem;                      // [2][A_STAGE]
@@ -316,10 +429,8 @@ gemm_kernel(KernelArgs p)
     int tm, tn;
     tile_coords(p, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
-
-    const int nkb = (p.K + BK - 1) / BK;
-    const int kbeg = blockIdx.z * p.kblocks_per_split;
-    const int kend = min(nkb, kbeg + p.kblocks_per_split);
+    int kbeg, kend;
+    split_range(p, BK, blockIdx.z, kbeg, kend);
 
     ALoader la;
     BLoader lb;
@@ -329,14 +440,8 @@ gemm_kernel(KernelArgs p)
         la.init(p.A, p.lda, m0, p.M, kbeg, tid);
     lb.init(p.B, p.ldb, n0, p.N, kbeg, tid);
 
-    f32x16 acc[G::RM][G::RN];
-#pragma unroll
-    for (int i = 0; i < G::RM; ++i)
-#pragma unroll
-        for (int j = 0; j < G::RN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
+    typename G::Acc acc;
+    G::zero(acc);
     typename ALoader::VT ra[ALoader::LOADS];
     typename BLoader::VT rb[BLoader::LOADS];
 
@@ -350,49 +455,13 @@ gemm_kernel(KernelArgs p)
     }
     __syncthreads();
 
-    // Fragment addressing (per lane) inside one stage.
-    // A staged k-contiguous: row (wm*WM + i*32 + l32), k from h*HALF.
-    // A staged m-contiguous: element [k][wm*WM + i*32 + l32].
     const int a_row = wm * G::WM + l32;
     const int b_row = wn * G::WN + l32;
 
-    // One group = 4 k-steps of the K-block (4 MFMAs per accumulator block).
     // Operand registers hold two groups: the one being multiplied and the
     // next one, read from LDS while the current MFMAs run.
-    float fa[2][G::RM][4], fb[2][G::RN][4];
-    auto read_group = [&](const float *as, const float *bs, int g, float (&xa)[G::RM][4],
-                          float (&xb)[G::RN][4]) {
-        const int k0 = h * G::HALF + 4 * g;
-#pragma unroll
-        for (int i = 0; i < G::RM; ++i) {
-            if constexpr (G::A_K) {
-                const f32x4 v = *reinterpret_cast<const f32x4 *>(as + (a_row + i * 32) * G::LDA_S + k0);
-                xa[i][0] = v[0]; xa[i][1] = v[1]; xa[i][2] = v[2]; xa[i][3] = v[3];
-            } else {
-#pragma unroll
-                for (int t = 0; t < 4; ++t) xa[i][t] = as[(k0 + t) * G::LDA_S + a_row + i * 32];
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < G::RN; ++j) {
-            if constexpr (B_KCONTIG) {
-                const f32x4 v = *reinterpret_cast<const f32x4 *>(bs + (b_row + j * 32) * G::LDB_S + k0);
-                xb[j][0] = v[0]; xb[j][1] = v[1]; xb[j][2] = v[2]; xb[j][3] = v[3];
-            } else {
-#pragma unroll
-                for (int t = 0; t < 4; ++t) xb[j][t] = bs[(k0 + t) * G::LDB_S + b_row + j * 32];
-            }
-        }
-    };
-    auto mma_group = [&](const float (&xa)[G::RM][4], const float (&xb)[G::RN][4]) {
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int i = 0; i < G::RM; ++i)
-#pragma unroll
-                for (int j = 0; j < G::RN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(xa[i][t], xb[j][t], acc[i][j], 0, 0, 0);
-    };
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
 
     // Software pipeline over K-blocks (two LDS stages):
     //   issue the global loads of block kb+1;
@@ -402,9 +471,9 @@ gemm_kernel(KernelArgs p)
     // Every read of a stage precedes the barrier that follows it, and every
     // write of a stage follows the barrier that ends the reads of its previous
     // contents, so one barrier per K-block orders both.
-    constexpr int NG = G::HALF / 4;
+    constexpr int NG = G::NG;
     int stage = 0;
-    if (kbeg < kend) read_group(As, Bs, 0, fa[0], fb[0]);
+    if (kbeg < kend) G::read_group(As, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
     for (int kb = kbeg; kb < kend; ++kb) {
         const bool more = kb + 1 < kend;
         if (more) {
@@ -417,9 +486,9 @@ gemm_kernel(KernelArgs p)
         const float *bs = Bs + stage * G::B_STAGE;
 #pragma unroll
         for (int g = 0; g < NG - 1; ++g) {
-            read_group(as, bs, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            G::read_group(as, bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
             __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of these MFMAs
-            mma_group(fa[g & 1], fb[g & 1]);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
         }
         if (more) {
             la.template store<G::LDA_S>(As + (stage ^ 1) * G::A_STAGE, ra, tid);
@@ -429,50 +498,158 @@ gemm_kernel(KernelArgs p)
         // unconditional (after the last block it reads stale LDS that is never
         // used): a conditional read would make the compiler copy registers
         // between the read and the MFMAs below
-        read_group(As + (stage ^ 1) * G::A_STAGE, Bs + (stage ^ 1) * G::B_STAGE, 0, fa[0], fb[0]);
+        G::read_group(As + (stage ^ 1) * G::A_STAGE, Bs + (stage ^ 1) * G::B_STAGE, a_row, b_row, h, 0, fa[0], fb[0]);
         __builtin_amdgcn_sched_barrier(0);
-        mma_group(fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
+        G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
         stage ^= 1;
     }
 
-    // Epilogue: C = alpha * acc (+ beta * C), or the split's partial sum.
-    const int col_base = n0 + wn * G::WN + l32;
-    const int row_base = m0 + wm * G::WM + 4 * h;
-    if (p.splits > 1) {
-        float *out = p.ws + (int64_t)blockIdx.z * p.M * p.N;
-#pragma unroll
-        for (int i = 0; i < G::RM; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
-                if (row < p.M) {
-#pragma unroll
-                    for (int j = 0; j < G::RN; ++j) {
-                        const int col = col_base + j * 32;
-                        if (col < p.N) out[(int64_t)row * p.N + col] = p.alpha * acc[i][j][r];
-                    }
-                }
-            }
-        return;
+    G::store(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+}
+
+// The items (split z, tile) of a persistent launch: item = z * tiles + tile.
+// Each XCD owns a contiguous share of the items (split as evenly as the item
+// count allows) and the work-groups resident on it walk that share with a
+// stride equal to their number, so at any time an XCD's L2 serves
+// neighbouring tiles.  Work-group b runs on XCD b % xcds; the share is only
+// used when the grid divides evenly among the XCDs.
+struct ItemWalk {
+    int cur, end, stride;
+
+    __device__ __forceinline__ void init(int items, int xcds)
+    {
+        const int G = gridDim.x, b = blockIdx.x;
+        const int X = (xcds > 1 && G % xcds == 0) ? xcds : 1;
+        const int x = b % X, w = b / X;
+        const int q = items / X, r = items % X;
+        const int start = x * q + min(x, r);
+        end = start + q + (x < r ? 1 : 0);
+        stride = G / X;
+        cur = start + w;
     }
-#pragma unroll
-    for (int i = 0; i < G::RM; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
-            if (row < p.M) {
-                float *crow = p.C + (int64_t)row * p.ldc;
-#pragma unroll
-                for (int j = 0; j < G::RN; ++j) {
-                    const int col = col_base + j * 32;
-                    if (col < p.N) {
-                        float v = p.alpha * acc[i][j][r];
-                        if (p.beta != 0.f) v = fmaf(p.beta, crow[col], v);
-                        crow[col] = v;
-                    }
-                }
-            }
+    __device__ __forceinline__ bool valid() const { return cur < end; }
+    __device__ __forceinline__ void next() { cur += stride; }
+};
+
+
+// Persistent form of gemm_kernel: a grid sized to what the CUs hold at once,
+// each work-group looping over its items.  The K-block pipeline runs across
+// item boundaries: the first block of the next item is loaded and staged
+// while the last block of the current one computes, and the epilogue's stores
+// overlap the next item's MFMAs, so short reductions (K of one to a few
+// blocks) no longer pay a load latency per tile.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_persistent_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
+    typedef typename G::ALoader ALoader;
+    typedef typename G::BLoader BLoader;
+
+    __shared__ __attribute__((aligned(16))) float smem[G::LDS_FLOATS];
+    float *As = smem;
+    float *Bs = smem + 2 * G::A_STAGE;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+    const int tiles = p.tiles_m * p.tiles_n;
+
+    ItemWalk walk;
+    walk.init(tiles * p.splits, p.xcds);
+    if (!walk.valid()) return;  // uniform over the work-group, before any barrier
+
+    int m0, n0, z, kb, kend;
+    auto decode = [&](int item, int &m0_, int &n0_, int &z_, int &kbeg_, int &kend_) {
+        z_ = item / tiles;
+        int tm, tn;
+        tile_of(p, item - z_ * tiles, tm, tn);
+        m0_ = tm * BM;
+        n0_ = tn * BN;
+        split_range(p, BK, z_, kbeg_, kend_);
+    };
+    decode(walk.cur, m0, n0, z, kb, kend);
+
+    ALoader la;
+    BLoader lb;
+    auto init_loaders = [&](int m0_, int n0_, int kbeg_) {
+        if constexpr (AMODE == A_CONV)
+            la.init(p, m0_, kbeg_, tid);
+        else
+            la.init(p.A, p.lda, m0_, p.M, kbeg_, tid);
+        lb.init(p.B, p.ldb, n0_, p.N, kbeg_, tid);
+    };
+    init_loaders(m0, n0, kb);
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename ALoader::VT ra[ALoader::LOADS];
+    typename BLoader::VT rb[BLoader::LOADS];
+
+    la.load(ra, kb * BK, p.K);
+    lb.load(rb, kb * BK, p.K);
+    la.advance();
+    lb.advance();
+    la.template store<G::LDA_S>(As, ra, tid);
+    lb.template store<G::LDB_S>(Bs, rb, tid);
+    __syncthreads();
+
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NG = G::NG;
+    int stage = 0;
+    G::read_group(As, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
+
+    // The same one-barrier pipeline as gemm_kernel, over the sequence of
+    // (item, K-block) pairs this work-group owns.
+    for (;;) {
+        const bool last_block = kb + 1 >= kend;
+        int nm0 = m0, nn0 = n0, nz = z, nkb = kb + 1, nkend = kend;
+        bool more = true;
+        if (last_block) {
+            walk.next();
+            more = walk.valid();
+            if (more) decode(walk.cur, nm0, nn0, nz, nkb, nkend);
         }
+        if (more) {
+            if (last_block) init_loaders(nm0, nn0, nkb);
+            la.load(ra, nkb * BK, p.K);
+            lb.load(rb, nkb * BK, p.K);
+            la.advance();
+            lb.advance();
+        }
+        const float *as = As + stage * G::A_STAGE;
+        const float *bs = Bs + stage * G::B_STAGE;
+#pragma unroll
+        for (int g = 0; g < NG - 1; ++g) {
+            G::read_group(as, bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        if (more) {
+            la.template store<G::LDA_S>(As + (stage ^ 1) * G::A_STAGE, ra, tid);
+            lb.template store<G::LDB_S>(Bs + (stage ^ 1) * G::B_STAGE, rb, tid);
+        }
+        __syncthreads();
+        G::read_group(As + (stage ^ 1) * G::A_STAGE, Bs + (stage ^ 1) * G::B_STAGE, a_row, b_row, h, 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
+        if (last_block) {
+            G::store(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, z);
+            G::zero(acc);
+        }
+        if (!more) break;
+        m0 = nm0;
+        n0 = nn0;
+        z = nz;
+        kb = nkb;
+        kend = nkend;
+        stage ^= 1;
+    }
 }
 
 }  // namespace pk

@@ -173,3 +173,63 @@ RESNET_ALT = ConvCase("resnet50 b32 28x28x512->128 1x1", 32, 28, 28, 512, 1, 1, 
 # The benchmark's step: the three 4096^3 GEMMs and the ten conv layers.
 STEP_GEMMS = GEMM_SWEEP[2:]
 STEP_CONVS = VGG_LAYERS + RESNET_LAYERS
+
+
+# ---------------------------------------------------------------- suites
+# Every distinct convolution layer of the paper's VGG-16 and ResNet-50
+# tables: (name, window, stride, input H (= W), Cin, Cout, pads t/l/b/r).
+# The pads are "same" padding written out (3x3 stride 1: one pixel all
+# round; 3x3 stride 2: the odd pixel at the bottom/right; 1x1: none) and none
+# for the 7x7 stride-2 first ResNet layer, whose 230 x 230 input is the
+# 224 x 224 image already padded by 3.
+_SAME3 = (1, 1, 1, 1)
+_SAME3S2 = (0, 0, 1, 1)
+_NONE = (0, 0, 0, 0)
+VGG16_TABLE = [
+    ("conv1_1", 3, 1, 224, 3, 64, _SAME3), ("conv1_2", 3, 1, 224, 64, 64, _SAME3),
+    ("conv2_1", 3, 1, 112, 64, 128, _SAME3), ("conv2_2", 3, 1, 112, 128, 128, _SAME3),
+    ("conv3_1", 3, 1, 56, 128, 256, _SAME3), ("conv3_2", 3, 1, 56, 256, 256, _SAME3),
+    ("conv4_1", 3, 1, 28, 256, 512, _SAME3), ("conv4_2", 3, 1, 28, 512, 512, _SAME3),
+    ("conv5_1", 3, 1, 14, 512, 512, _SAME3),
+]
+RESNET50_TABLE = [
+    ("conv1_1", 7, 2, 230, 3, 64, _NONE),
+    ("conv2_1", 1, 1, 56, 64, 256, _NONE), ("conv2_2", 1, 1, 56, 64, 64, _NONE),
+    ("conv2_3", 3, 1, 56, 64, 64, _SAME3), ("conv2_4", 1, 1, 56, 256, 64, _NONE),
+    ("conv2_5", 3, 2, 56, 64, 64, _SAME3S2),
+    ("conv3_1", 1, 1, 28, 64, 256, _NONE), ("conv3_2", 1, 1, 28, 256, 512, _NONE),
+    ("conv3_3", 1, 1, 28, 256, 128, _NONE), ("conv3_4", 3, 1, 28, 128, 128, _SAME3),
+    ("conv3_5", 1, 1, 28, 128, 512, _NONE), ("conv3_6", 1, 1, 28, 512, 128, _NONE),
+    ("conv3_7", 3, 2, 28, 128, 128, _SAME3S2),
+    ("conv4_1", 1, 1, 14, 128, 512, _NONE), ("conv4_2", 1, 1, 14, 512, 1024, _NONE),
+    ("conv4_3", 1, 1, 14, 512, 256, _NONE), ("conv4_4", 3, 1, 14, 256, 256, _SAME3),
+    ("conv4_5", 1, 1, 14, 256, 1024, _NONE), ("conv4_6", 1, 1, 14, 1024, 256, _NONE),
+    ("conv4_7", 3, 2, 14, 256, 256, _SAME3S2),
+    ("conv5_1", 1, 1, 7, 256, 1024, _NONE), ("conv5_2", 1, 1, 7, 1024, 2048, _NONE),
+    ("conv5_3", 1, 1, 7, 1024, 512, _NONE), ("conv5_4", 3, 1, 7, 512, 512, _SAME3),
+    ("conv5_5", 1, 1, 7, 512, 2048, _NONE), ("conv5_6", 1, 1, 7, 2048, 512, _NONE),
+]
+
+
+def layer_suite(batch: int):
+    """Every distinct layer of both tables at the given batch, as ConvCases."""
+    cases = []
+    for net, table, seed0 in (("vgg16", VGG16_TABLE, 100), ("resnet50", RESNET50_TABLE, 200)):
+        for i, (name, k, s, hw, cin, cout, pads) in enumerate(table):
+            cases.append(ConvCase("%s %s b%d %dx%dx%d->%d %dx%d s%d" % (net, name, batch, hw, hw, cin, cout, k, k, s),
+                                  batch, hw, hw, cin, k, k, cout, (s, s), pads, seed0 + 1000 * batch + i))
+    return cases
+
+
+# The paper's GEMM sweep: M, N, K each a power of two in [64, 1024].
+SWEEP_SIZES = (64, 128, 256, 512, 1024)
+
+
+def gemm_sweep():
+    cases = []
+    for M in SWEEP_SIZES:
+        for N in SWEEP_SIZES:
+            for K in SWEEP_SIZES:
+                cases.append(GemmCase("gemm NN %dx%dx%d" % (M, N, K), "N", "N", M, N, K, 1.0, 0.0,
+                                      7000 + M + 3 * N + 7 * K))
+    return cases

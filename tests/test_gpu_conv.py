@@ -178,3 +178,63 @@ def test_conv_batch_zero_and_errors():
     st = pk.binding.conv2d_fwd_raw(xx.data_ptr(), 1, 5, 5, 4, f.data_ptr(), 3, 3, 4, 1, 1, 1, 1, 1, 1,
                                    xx.data_ptr(), 5, 5)  # output aliases input
     assert st == 1 and pk.last_invalid_param() == 16
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+def test_persistent_conv_configs_loop_over_tiles(splits):
+    """Persistent convolution configurations with several tiles (and split-K
+    items) per resident work-group; NaN-prefilled output, sampled bit-exact
+    parity on integer data."""
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(90 + splits)
+    N, H, W, Cin, Cout = 16, 96, 96, 16, 68
+    x = wl.integers(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+    f = wl.integers(rng, 9 * Cin * Cout).reshape(3, 3, Cin, Cout)
+    dx, df = dev(x), dev(f)
+    ws = torch.empty(splits * N * H * W * Cout, dtype=torch.float32, device="cuda")
+    idx = sample_conv_outputs(N, H, W, Cout, 4000, splits)
+    ref, _ = oracle.conv2d_at(x, f, (1, 1), (1, 1, 1, 1), idx)
+    for cfg in pk.configs():
+        if cfg["kind"] != 1 or not cfg["persistent"]:
+            continue
+        y = torch.full((N, H, W, Cout), float("nan"), dtype=torch.float32, device="cuda")
+        pk.force_config(cfg["name"])
+        pk.force_splits(splits)
+        try:
+            pk.conv2d_fwd(dx, df, padding=(1, 1, 1, 1), out=y, workspace=ws)
+            used = pk.last_config_name()
+        finally:
+            pk.force_config(None)
+            pk.force_splits(0)
+        assert used == cfg["name"]
+        out = host(y)
+        assert np.all(np.isfinite(out)), cfg["name"]
+        assert np.array_equal(out.reshape(-1)[idx].astype(np.float64), ref), cfg["name"]
+
+
+SUITE = [(b, c) for b in (1, 4, 32) for c in wl.layer_suite(b)]
+
+
+@pytest.mark.parametrize("batch,case", SUITE, ids=[c.name for _, c in SUITE])
+def test_paper_layer_suite(batch, case):
+    """Every distinct VGG-16 / ResNet-50 layer of the paper at batch 1, 4, 32:
+    the whole output where the oracle is quick, else sampled outputs (every
+    border class included)."""
+    torch, pk = require_gpu()
+    x, f = case.inputs()
+    N, H, W, Cin = case.x_shape
+    KH, KW, _, Cout = case.f_shape
+    wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
+    ws = torch.empty(max(wsb // 4, 1), dtype=torch.float32, device="cuda") if wsb else None
+    out, cfg = _run(pk, x, f, case.stride, case.pads, workspace=ws)
+    Ho, Wo = oracle.conv2d_out_dims(H, W, KH, KW, *case.stride, *case.pads)
+    assert out.shape == (N, Ho, Wo, Cout)
+    macs = N * Ho * Wo * Cout * KH * KW * Cin
+    if macs <= 4e8:
+        ref, scale = oracle.conv2d(x, f, case.stride, case.pads)
+        assert_parity(out, ref, scale, case.name + " " + cfg)
+    else:
+        idx = sample_conv_outputs(N, Ho, Wo, Cout, 3000, case.seed)
+        ref, scale = oracle.conv2d_at(x, f, case.stride, case.pads, idx)
+        assert_parity(out.reshape(-1)[idx], ref, scale, case.name + " " + cfg)
+    assert np.all(np.isfinite(out))

@@ -177,3 +177,47 @@ def test_column_major_swap_identity():
     # the oracle on the same problem stated row-major: A_cm is A^T, B_cm is B^T
     ref, _ = oracle.sgemm("T", "T", M, N, K, 1.0, A_cm, M, B_cm, K, 0.0, np.zeros((M, N), np.float32), N)
     assert np.array_equal(C_cm.T.astype(np.float64), ref)
+
+
+def test_persistent_configs_loop_over_tiles():
+    """Persistent configurations on products with several tiles per resident
+    work-group: C starts as NaN with beta = 0, so an unwritten tile shows; the
+    sampled outputs (tile corners included) must equal the oracle bit for bit
+    on integer data."""
+    torch, pk = require_gpu()
+    for cfg in pk.configs():
+        if cfg["kind"] != 0 or not cfg["persistent"]:
+            continue
+        ta = "T" if cfg["trans_a"] else "N"
+        tb = "T" if cfg["trans_b"] else "N"
+        M, N, K = cfg["bm"] * 32, cfg["bn"] * 64 + 4, 44  # ragged last column of tiles
+        rng = np.random.default_rng(cfg["bm"] + cfg["bn"])
+        A = wl.integers(rng, M * K).reshape((K, M) if ta == "T" else (M, K))
+        B = wl.integers(rng, K * N).reshape((N, K) if tb == "T" else (K, N))
+        dA, dB = dev(A), dev(B)
+        dC = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        pk.force_config(cfg["name"])
+        try:
+            pk.gemm(dA, dB, dC, trans_a=ta == "T", trans_b=tb == "T")
+            used = pk.last_config_name()
+        finally:
+            pk.force_config(None)
+        assert used == cfg["name"]
+        out = host(dC)
+        assert np.all(np.isfinite(out)), cfg["name"]
+        rows, cols = sample_rows_cols(M, N, 4000, 5, tiles=(cfg["bm"], cfg["bn"]))
+        ref, _ = oracle.sgemm_at(ta, tb, M, N, K, 1.0, A, A.shape[1], B, B.shape[1], 0.0,
+                                 np.zeros((1, 1), np.float32), N, rows, cols)
+        assert np.array_equal(out[rows, cols].astype(np.float64), ref), cfg["name"]
+
+
+@pytest.mark.parametrize("case", wl.gemm_sweep(), ids=lambda c: c.name)
+def test_paper_gemm_sweep(case):
+    """The paper's sweep (M, N, K powers of two in [64, 1024]), whole outputs."""
+    torch, pk = require_gpu()
+    A, B, C = case.inputs()
+    dC = dev(np.full_like(C, np.nan))
+    pk.gemm(dev(A), dev(B), dC)
+    out = host(dC)
+    ref, scale = oracle.sgemm("N", "N", case.M, case.N, case.K, 1.0, A, case.lda, B, case.ldb, 0.0, C, case.ldc)
+    assert_parity(out, ref, scale, case.name + " " + pk.last_config_name())
