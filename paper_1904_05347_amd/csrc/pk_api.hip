@@ -156,17 +156,17 @@ const TunedShape kTuned[] = {
     {0, 0, 0, 2048, 2048, 2048, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
     {0, 0, 0, 1024, 1024, 1024, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
     // VGG-16 block-first layers at batch 32 (3x3, stride 1)
-    {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2", 1},
-    {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_64x64x32_w2x2_v44", 1},
+    {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
+    {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
     {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44", 1},
-    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44", 2},
+    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 3},
     // ResNet-50 bottleneck layers at batch 32
     {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},
-    {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x32_w2x4_v44_o2", 1},
+    {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x64_w2x4_v44_o2", 1},
     {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
     {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
-    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 3},
-    {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x64x32_w2x2_nn_v44", 1},
+    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 4},
+    {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 1},
 };
 
 const TunedShape *find_tuned(int kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t kh, int64_t stride)

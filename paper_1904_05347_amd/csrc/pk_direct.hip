@@ -33,9 +33,16 @@ constexpr int DT_ROWS_PER_WAVE = DT_ROWS / DT_WAVES;
 constexpr int DT_KMAX = 32;      // longest reduction this kernel takes
 constexpr int DT_LDS_FLOATS = 12 * 1024;  // input patch capacity (48 KiB)
 
+// Floats of the input patch a work-group stages: the launch sizes LDS to it,
+// so small patches leave room for more resident work-groups.
+int64_t direct_patch_floats(int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t sw)
+{
+    return ((DT_ROWS - 1) * sh + KH) * ((DT_COLS - 1) * sw + KW) * Cin;
+}
+
 __global__ void __launch_bounds__(64 * DT_WAVES) direct_conv_kernel(KernelArgs p)
 {
-    __shared__ float patch[DT_LDS_FLOATS];
+    extern __shared__ float patch[];  // direct_patch_floats() floats
     const float *x = p.A;
     const float *f = p.B;
     float *y = p.C;
@@ -100,6 +107,7 @@ __global__ void __launch_bounds__(64 * DT_WAVES) direct_conv_kernel(KernelArgs p
             for (int i = 0; i < 16; ++i) acc[r][j][i] = 0.f;
 
     const int ksteps = (K + 1) / 2;
+    const bool tail_lane = (K & 1) && h == 1;
 #pragma unroll
     for (int r = 0; r < DT_ROWS_PER_WAVE; ++r) {
         const int prow = (wave * DT_ROWS_PER_WAVE + r) * sh;     // patch row of tap kh = 0
@@ -107,7 +115,10 @@ __global__ void __launch_bounds__(64 * DT_WAVES) direct_conv_kernel(KernelArgs p
 #pragma unroll
         for (int s = 0; s < DT_KMAX / 2; ++s) {
             if (s < ksteps) {
-                const float a = base[off[s]];
+                // for odd K the upper half-wave's last k is past the window:
+                // its filter value is 0 and its input value must be 0 too
+                // (an infinite input would otherwise give 0 * inf = NaN)
+                const float a = (s == ksteps - 1 && tail_lane) ? 0.f : base[off[s]];
                 acc[r][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv[0][s], acc[r][0], 0, 0, 0);
                 acc[r][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv[1][s], acc[r][1], 0, 0, 0);
             }
@@ -137,7 +148,8 @@ hipError_t launch_direct(const KernelArgs &a, hipStream_t stream)
 {
     const unsigned tiles = (unsigned)(((a.Ho + DT_ROWS - 1) / DT_ROWS) * ((a.Wo + DT_COLS - 1) / DT_COLS));
     const dim3 grid(tiles, (unsigned)a.batch, (unsigned)((a.N + DT_CH - 1) / DT_CH));
-    hipLaunchKernelGGL(direct_conv_kernel, grid, dim3(64 * DT_WAVES), 0, stream, a);
+    const size_t lds = (size_t)direct_patch_floats(a.KH, a.KW, a.Cin, a.sh, a.sw) * sizeof(float);
+    hipLaunchKernelGGL(direct_conv_kernel, grid, dim3(64 * DT_WAVES), lds, stream, a);
     return hipGetLastError();
 }
 
@@ -147,8 +159,7 @@ bool direct_conv_fits(int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t s
 {
     if (KH > DT_KMAX || KW > DT_KMAX || Cin > DT_KMAX || sh > 64 || sw > 64) return false;
     if (KH * KW * Cin > DT_KMAX) return false;
-    const int64_t ph = (DT_ROWS - 1) * sh + KH, pw = (DT_COLS - 1) * sw + KW;
-    return ph * pw * Cin <= DT_LDS_FLOATS;
+    return direct_patch_floats(KH, KW, Cin, sh, sw) <= DT_LDS_FLOATS;
 }
 
 const Config *configs_direct(int *count)
