@@ -15,7 +15,11 @@ What pins what:
     an edge and 4*Cin at a corner of a 3x3 stride-1 "same" convolution);
   - invariants (1x1 convolution == GEMM, im2col product, (AB)^T = B^T A^T);
   - a textbook routine: torch's CPU float64 matmul and conv2d;
-  - the paper's layer tables (output sizes from window and stride).
+  - the paper's layer tables (output sizes from window and stride);
+  - Winograd F(2x2, 3x3) (Section 4.1.2): its value against the exact
+    brute-force convolution (it is the same function in exact arithmetic),
+    bit-equality with the direct sum on small integers, and its error scale
+    against a hand-derived closed form and the direct scale it must bound.
 """
 from __future__ import annotations
 
@@ -393,6 +397,60 @@ def pin_same_padding_property(orc):
                         assert span < 0 or span // s + 1 < -(-n // s)
 
 
+# -------------------------------------------- Winograd F(2x2, 3x3) (Section 4.1.2)
+
+def pin_winograd_brute_force(orc):
+    """The transformed computation is the convolution: equal to the exact
+    brute-force result up to fp64 rounding, with ragged 2x2 tiles (odd output
+    sizes) and asymmetric padding."""
+    rng = _rng(17)
+    for H, W in [(3, 3), (4, 5), (5, 4), (6, 7)]:
+        for pads in [(0, 0, 0, 0), (1, 1, 1, 1), (2, 0, 1, 2), (0, 2, 2, 1)]:
+            if H + pads[0] + pads[2] < 3 or W + pads[1] + pads[3] < 3:
+                continue
+            x = _grid_uniform(rng, (2, H, W, 3))
+            f = _grid_uniform(rng, (3, 3, 3, 2))
+            exp, _ = brute_conv(x, f, (1, 1), pads)
+            ref, scale = orc.winograd_f2x3(x, f, pads)
+            assert ref.shape == exp.shape, (H, W, pads, ref.shape, exp.shape)
+            err = np.abs(ref - exp)
+            assert np.all(err <= 1e-13 * scale), (H, W, pads, float(np.max(err)))
+
+
+def pin_winograd_integer_exact(orc):
+    """On small integers every intermediate of the transformed computation is
+    a multiple of 1/4 far below 2^53: it must equal the direct sum exactly."""
+    rng = _rng(19)
+    x = rng.integers(-8, 9, size=(2, 7, 6, 5)).astype(np.float32)
+    f = rng.integers(-8, 9, size=(3, 3, 5, 4)).astype(np.float32)
+    for pads in [(1, 1, 1, 1), (0, 0, 0, 0), (2, 1, 0, 2)]:
+        ref_d, _ = orc.conv2d(x, f, (1, 1), pads)
+        ref_w, _ = orc.winograd_f2x3(x, f, pads)
+        assert np.array_equal(ref_w, ref_d), pads
+
+
+def pin_winograd_scale(orc):
+    """The error scale: on all-ones data without padding every output is
+    (4 Cin) * (sum of |G| row sums over the three rows |AT| selects)^2 =
+    4 Cin * (1 + 3/2 + 3/2)^2 = 64 Cin (|BT| rows each sum to 2, the rows of
+    |G| to 1, 3/2, 3/2, 1); on random data it bounds the direct sum |a*b|
+    from above, as every product of the direct sum appears in its expansion
+    with total coefficient at least 1."""
+    for C in (1, 3, 8):
+        x = np.ones((1, 6, 8, C), dtype=np.float32)
+        f = np.ones((3, 3, C, 2), dtype=np.float32)
+        ref, scale = orc.winograd_f2x3(x, f, (0, 0, 0, 0))
+        assert np.all(ref == 9 * C) and np.all(scale == 64 * C), C
+    rng = _rng(23)
+    x = _grid_uniform(rng, (2, 9, 7, 4))
+    f = _grid_uniform(rng, (3, 3, 4, 3))
+    for pads in [(1, 1, 1, 1), (0, 0, 0, 0), (2, 0, 1, 2)]:
+        _, t = orc.conv2d(x, f, (1, 1), pads)
+        _, tw = orc.winograd_f2x3(x, f, pads)
+        assert np.all(tw >= t * (1 - 1e-12)), pads
+
+
 ALL_PINS = [pin_gemm_brute_force, pin_conv_brute_force, pin_gemm_identity_permutation,
             pin_conv_delta_filters, pin_all_ones_closed_forms, pin_invariants,
-            pin_torch_float64, pin_layer_tables, pin_same_padding_property]
+            pin_torch_float64, pin_layer_tables, pin_same_padding_property,
+            pin_winograd_brute_force, pin_winograd_integer_exact, pin_winograd_scale]

@@ -33,6 +33,16 @@ MUTATIONS = {
     "same pads extra on top": ("pads_tlbr[0] = ph / 2;", "pads_tlbr[0] = ph - ph / 2;"),
     "same size floor": ("int64_t ho = (H + sh - 1) / sh, wo = (W + sw - 1) / sw;",
                         "int64_t ho = H / sh, wo = W / sw;"),
+    "winograd BT row sign": ("{0, -1, 1, 0}, {0, 1, 0, -1}}", "{0, 1, -1, 0}, {0, 1, 0, -1}}"),
+    "winograd G half dropped": ("{0.5, -0.5, 0.5}", "{1, -1, 1}"),
+    "winograd AT last entry": ("{0, 1, -1, -1}}", "{0, 1, -1, 1}}"),
+    "winograd tile origin uses left pad": ("ih0 = 2 * th - p->pt", "ih0 = 2 * th - p->pl"),
+    "winograd tile stride 1": ("iw0 = 2 * tw - p->pl", "iw0 = tw - p->pl"),
+    "winograd last channel dropped": ("for (int64_t ch = 0; ch < p->C; ++ch)", "for (int64_t ch = 0; ch + 1 < p->C; ++ch)"),
+    "winograd scale without abs on AT": ("ya += fabs(WG_AT[i][a]) * ma[a][b] * fabs(WG_AT[j][b]);",
+                                          "ya += WG_AT[i][a] * ma[a][b] * WG_AT[j][b];"),
+    "winograd filter scale without abs": ("ua += fabs(WG_G[a][r]) * fabs(g[r][c]) * fabs(WG_G[b][c]);",
+                                          "ua += fabs(WG_G[a][r]) * g[r][c] * fabs(WG_G[b][c]);"),
 }
 
 
