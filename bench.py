@@ -41,10 +41,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
-    ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep"),
+    ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep", "winograd"),
                     help="step: the benchmark step (default); layers: every VGG-16 / ResNet-50 layer of the "
                          "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
-                         "the vendor fp32 GEMM beside it")
+                         "the vendor fp32 GEMM beside it; winograd: the 3x3 stride-1 layers through the "
+                         "Winograd F(2x2, 3x3) path beside the default path")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
                          "the HBM copy bandwidth and the vendor fp32 GEMM at 4096^3, print one JSON line")
@@ -231,6 +232,45 @@ def run_layer_suite(torch, pk, wl):
     return {"suite": "layers", "dtype": "f32", "data": "synthetic", "rows": rows}
 
 
+def run_winograd_suite(torch, pk, wl):
+    """Every 3x3 stride-1 layer of the paper's tables at batch 1, 4, 32: the
+    Winograd F(2x2, 3x3) path beside the default (implicit-GEMM) path.
+    TFLOP/s are nominal (the direct sum's 2*N*Ho*Wo*Cout*9*Cin over the time);
+    product_tflops counts the 16 batched products the Winograd path runs."""
+    rows = []
+    for batch in (1, 4, 32):
+        for case in wl.layer_suite(batch):
+            KH, KW, Cin, Cout = case.f_shape
+            if (KH, KW) != (3, 3) or case.stride != (1, 1):
+                continue
+            x, f = case.inputs()
+            N, H, W, _ = case.x_shape
+            Ho, Wo = pk.conv2d_out_dims(H, W, 3, 3, 1, 1, *case.pads)
+            dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+            dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+            wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, 3, 3, Cout, 1, 1, *case.pads)
+            ws = torch.empty(wsb // 4, dtype=torch.float32, device="cuda") if wsb else None
+            wwb = pk.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, *case.pads)
+            wws = torch.empty(wwb // 4, dtype=torch.float32, device="cuda")
+            ms_d = _time_ms(torch, lambda: pk.conv2d_fwd(dx, df, padding=case.pads, out=dy, workspace=ws))
+            cfg_d = pk.last_config_name()
+            ms_w = _time_ms(torch, lambda: pk.conv2d_winograd(dx, df, padding=case.pads, out=dy, workspace=wws))
+            cfg_w = pk.last_config_name()
+            flops = wl.conv_flops(case, Ho, Wo)
+            tiles = N * ((Ho + 1) // 2) * ((Wo + 1) // 2)
+            prod_flops = 16 * 2 * tiles * Cin * Cout
+            rows.append({"layer": case.name, "config_direct": cfg_d, "config_winograd": cfg_w,
+                         "ms_direct": round(ms_d, 4), "ms_winograd": round(ms_w, 4),
+                         "speedup": round(ms_d / ms_w, 3),
+                         "tflops_direct": round(flops / (ms_d * 1e-3) / 1e12, 2),
+                         "tflops_winograd_nominal": round(flops / (ms_w * 1e-3) / 1e12, 2),
+                         "product_tflops": round(prod_flops / (ms_w * 1e-3) / 1e12, 2)})
+            del dx, df, dy, ws, wws
+            print("bench: %s direct %.4f ms winograd %.4f ms" % (case.name, ms_d, ms_w), file=sys.stderr,
+                  flush=True)
+    return {"suite": "winograd", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
 def run_gemm_sweep(torch, pk, wl):
     """The paper's GEMM sweep (M, N, K powers of two in [64, 1024]), with the
     vendor fp32 GEMM (torch.matmul, tf32 off) timed beside it as context."""
@@ -305,6 +345,9 @@ def main():
         return
     if args.suite == "gemm-sweep":
         print(json.dumps(run_gemm_sweep(torch, pk, wl)))
+        return
+    if args.suite == "winograd":
+        print(json.dumps(run_winograd_suite(torch, pk, wl)))
         return
     print("bench: generating inputs", file=sys.stderr, flush=True)
     ops, host = make_ops(torch, pk, wl)

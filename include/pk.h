@@ -126,6 +126,37 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
                   float *y, int64_t Ho, int64_t Wo,
                   void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Winograd convolution F(2x2, 3x3) (Section 4.1.2, the transform technique
+ * the paper takes from Lavin and Gray): the same operation as pk_conv2d_fwd
+ * for a 3 x 3 window at stride 1, computed as
+ *   U = G g G^T per (ci, co) filter,  V = B^T d B per 4 x 4 input tile d and
+ *   channel,  M[p] = V[p] U[p] for the 16 positions p of the transformed
+ *   tile (one batched product, Cin deep),  y = A^T m A per 2 x 2 output block,
+ * with 2.25x fewer multiplications than the direct sum.  Its fp32 rounding
+ * differs from the direct sum's: each output is accurate to 1e-5 times the
+ * same chain evaluated on absolute values (matrix entries and operands).
+ *
+ * Arguments, layouts and argument positions of errors are those of
+ * pk_conv2d_fwd.  KH = KW = 3 and sh = sw = 1 are required (else
+ * PK_ERR_NOT_SUPPORTED); any padding >= 0.
+ *   workspace    REQUIRED device buffer, 16-byte aligned, of at least
+ *                pk_conv2d_winograd_workspace_bytes() bytes (else
+ *                PK_ERR_WORKSPACE; misaligned: PK_ERR_INVALID_VALUE at 19).
+ *                It holds the transformed filter, input and products;
+ *                contents on return are unspecified.  It must not overlap
+ *                x, f or y.
+ * pk_last_config_name() names the contraction configuration of the product.
+ */
+size_t pk_conv2d_winograd_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin,
+                                          int64_t Cout, int64_t pt, int64_t pl,
+                                          int64_t pb, int64_t pr);
+int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                           const float *f, int64_t KH, int64_t KW, int64_t Cout,
+                           int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb, int64_t pr,
+                           float *y, int64_t Ho, int64_t Wo,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static text for a status code. */
 const char *pk_status_string(int status);
 

@@ -59,6 +59,10 @@ SIGNATURES = {
     "pk_conv2d_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
                                      _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
                                      _p, ctypes.c_size_t, _p]),
+    "pk_conv2d_winograd_workspace_bytes": (ctypes.c_size_t, [_i64] * 9),
+    "pk_conv2d_winograd_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
+                                              _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
+                                              _p, ctypes.c_size_t, _p]),
     "pk_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "pk_last_invalid_param": (ctypes.c_int, []),
     "pk_last_config_name": (ctypes.c_char_p, []),
@@ -116,6 +120,17 @@ def conv2d_fwd_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, 
     """pk_conv2d_fwd on raw device addresses; returns the status code."""
     return load().pk_conv2d_fwd(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr,
                                 y, Ho, Wo, workspace, workspace_bytes, stream)
+
+
+def conv2d_winograd_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo,
+                        workspace, workspace_bytes, stream=None) -> int:
+    """pk_conv2d_winograd_fwd on raw device addresses; returns the status code."""
+    return load().pk_conv2d_winograd_fwd(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr,
+                                         y, Ho, Wo, workspace, workspace_bytes, stream)
+
+
+def conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr) -> int:
+    return load().pk_conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr)
 
 
 def conv2d_out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr):
@@ -310,4 +325,40 @@ def conv2d_fwd(x, w, stride=(1, 1), padding="SAME", out=None, workspace=None):
     st = conv2d_fwd_raw(x.data_ptr(), N, H, W, Cin, w.data_ptr(), KH, KW, Cout, sh, sw,
                         pt, pl, pb, pr, out.data_ptr(), Ho, Wo, ws_ptr, ws_bytes, _stream_handle(out))
     _check(st, "pk_conv2d_fwd")
+    return out
+
+
+def conv2d_winograd(x, w, padding="SAME", out=None, workspace=None):
+    """Winograd F(2x2, 3x3) convolution of NHWC x with a 3 x 3 HWIO w, stride 1.
+
+    Same result as ``conv2d_fwd`` up to fp32 rounding of the transforms.  The
+    workspace (float32 device tensor of at least
+    ``conv2d_winograd_workspace_bytes`` bytes) is allocated when None.
+    """
+    import torch
+    _check_f32_cuda(x, "x")
+    _check_f32_cuda(w, "w")
+    if x.dim() != 4 or w.dim() != 4:
+        raise ValueError("x is N x H x W x Cin, w is KH x KW x Cin x Cout")
+    if not x.is_contiguous() or not w.is_contiguous():
+        raise ValueError("x and w must be contiguous (NHWC / HWIO)")
+    N, H, W, Cin = x.shape
+    KH, KW, Cin2, Cout = w.shape
+    if Cin2 != Cin:
+        raise ValueError("input channels differ: %d vs %d" % (Cin, Cin2))
+    pt, pl, pb, pr = resolve_padding(padding, H, W, KH, KW, 1, 1)
+    Ho, Wo = conv2d_out_dims(H, W, KH, KW, 1, 1, pt, pl, pb, pr)
+    if out is None:
+        out = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device=x.device)
+    _check_f32_cuda(out, "out")
+    if tuple(out.shape) != (N, Ho, Wo, Cout) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous %s tensor" % ((N, Ho, Wo, Cout),))
+    if workspace is None:
+        need = conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr)
+        workspace = torch.empty(max(need // 4, 1), dtype=torch.float32, device=x.device)
+    _check_f32_cuda(workspace, "workspace")
+    st = conv2d_winograd_raw(x.data_ptr(), N, H, W, Cin, w.data_ptr(), KH, KW, Cout, 1, 1,
+                             pt, pl, pb, pr, out.data_ptr(), Ho, Wo, workspace.data_ptr(),
+                             workspace.numel() * 4, _stream_handle(out))
+    _check(st, "pk_conv2d_winograd_fwd")
     return out

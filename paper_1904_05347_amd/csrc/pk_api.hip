@@ -625,3 +625,154 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------ Winograd
+
+namespace {
+
+// Tiles of 2 x 2 outputs and the three workspace regions (256-byte aligned).
+struct WinoPlan {
+    int64_t Ho, Wo, TH, TW, T;
+    size_t off_u, off_v, off_m, bytes;
+};
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// false when the sizes overflow the kernels' indexing.
+bool wino_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Cin, int64_t Cout, WinoPlan *w)
+{
+    w->Ho = Ho;
+    w->Wo = Wo;
+    w->TH = (Ho + 1) / 2;
+    w->TW = (Wo + 1) / 2;
+    w->T = checked_mul3(N, w->TH, w->TW);
+    const int64_t u = checked_mul3(16, Cin, Cout), v = checked_mul3(16, w->T, Cin), m = checked_mul3(16, w->T, Cout);
+    if (w->T < 0 || u < 0 || v < 0 || m < 0 || w->T > kMaxDim) return false;
+    // transform grids: one thread per (tile, channel), < 2^31 work-groups of 256
+    if (w->T * Cin >= ((int64_t)1 << 38) || w->T * Cout >= ((int64_t)1 << 38) || Cin * Cout >= ((int64_t)1 << 38))
+        return false;
+    w->off_u = 0;
+    w->off_v = align256((size_t)u * sizeof(float));
+    w->off_m = w->off_v + align256((size_t)v * sizeof(float));
+    w->bytes = w->off_m + align256((size_t)m * sizeof(float));
+    return true;
+}
+
+// The batched product's configuration: a forced one (a non-persistent NN
+// GEMM instance), else by the size of the whole batch.
+const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok, bool *bad)
+{
+    const Config *c = forced(bad);
+    if (*bad) return nullptr;
+    if (c) return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent) ? c : nullptr;
+    if (!vec_ok) return find_config("gemm_64x64x16_w2x2_nn_v11");
+    const int64_t tiles128 = 16 * ceil_div(T, 128) * ceil_div(Cout, 128);
+    if (tiles128 >= 4 * kCUs && Cin >= 64) return find_config("gemm_128x128x32_w2x2_nn_v44");
+    return find_config(Cin <= 64 ? "gemm_64x64x16_w2x2_nn_v44" : "gemm_64x64x32_w2x2_nn_v44");
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t pk_conv2d_winograd_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, int64_t Cout, int64_t pt,
+                                          int64_t pl, int64_t pb, int64_t pr)
+{
+    int64_t Ho = 0, Wo = 0;
+    if (N < 1 || Cin < 1 || Cout < 1 || Cin > kMaxDim || Cout > kMaxDim) return 0;
+    const int saved = t_last_param;
+    const int st = out_dims(H, W, 3, 3, 1, 1, pt, pl, pb, pr, &Ho, &Wo, 2);
+    t_last_param = saved;
+    if (st != PK_OK) return 0;
+    WinoPlan w;
+    if (!wino_plan(N, Ho, Wo, Cin, Cout, &w)) return 0;
+    return w.bytes;
+}
+
+int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, const float *f, int64_t KH,
+                           int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb,
+                           int64_t pr, float *y, int64_t Ho, int64_t Wo, void *workspace, size_t workspace_bytes,
+                           void *stream)
+{
+    begin();
+    if (N < 0) return invalid(2);
+    if (H < 1) return invalid(3);
+    if (W < 1) return invalid(4);
+    if (Cin < 1) return invalid(5);
+    if (KH < 1) return invalid(7);
+    if (KW < 1) return invalid(8);
+    if (Cout < 1) return invalid(9);
+    if (sh < 1) return invalid(10);
+    if (sw < 1) return invalid(11);
+    if (pt < 0) return invalid(12);
+    if (pl < 0) return invalid(13);
+    if (pb < 0) return invalid(14);
+    if (pr < 0) return invalid(15);
+    int64_t ho = 0, wo = 0;
+    {
+        const int st = out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr, &ho, &wo, 2);
+        if (st == PK_ERR_INVALID_VALUE) {
+            static const int map[11] = {0, 3, 4, 7, 8, 10, 11, 12, 13, 14, 15};
+            return invalid(map[t_last_param]);
+        }
+        if (st != PK_OK) return st;
+    }
+    if (Ho != ho) return invalid(17);
+    if (Wo != wo) return invalid(18);
+    if (KH != 3 || KW != 3 || sh != 1 || sw != 1) return PK_ERR_NOT_SUPPORTED;
+    if (N == 0) return PK_OK;
+    if (!x) return invalid(1);
+    if (!f) return invalid(6);
+    if (!y) return invalid(16);
+    const int64_t pixels = checked_mul3(N, H, W);
+    if (pixels < 0 || N > kMaxDim || Cin > kMaxDim || Cout > kMaxDim || H * W > kMaxDim ||
+        checked_mul3(pixels, Cin, 1) < 0 || checked_mul3(checked_mul3(N, Ho, Wo), Cout, 1) < 0)
+        return PK_ERR_NOT_SUPPORTED;
+    WinoPlan w;
+    if (!wino_plan(N, Ho, Wo, Cin, Cout, &w)) return PK_ERR_NOT_SUPPORTED;
+    if (!workspace || workspace_bytes < w.bytes) return PK_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return invalid(19);
+
+    uintptr_t x0, x1, f0, f1, y0, y1;
+    span(x, pixels, Cin, Cin, &x0, &x1);
+    span(f, 9 * Cin, Cout, Cout, &f0, &f1);
+    span(y, N * Ho * Wo, Cout, Cout, &y0, &y1);
+    if (overlap(y0, y1, x0, x1) || overlap(y0, y1, f0, f1)) return invalid(16);
+    const uintptr_t w0 = (uintptr_t)workspace, w1 = w0 + w.bytes;
+    if (overlap(w0, w1, x0, x1) || overlap(w0, w1, f0, f1) || overlap(w0, w1, y0, y1)) return invalid(19);
+
+    float *U = (float *)((char *)workspace + w.off_u);
+    float *V = (float *)((char *)workspace + w.off_v);
+    float *Mm = (float *)((char *)workspace + w.off_m);
+    const bool in4 = Cin % 4 == 0 && aligned16(x);
+    const bool out4 = Cout % 4 == 0 && aligned16(y);
+    bool bad = false;
+    const Config *c = select_wino_gemm(w.T, Cout, Cin, Cin % 4 == 0 && Cout % 4 == 0, &bad);
+    if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
+    if (!c) return PK_ERR_NOT_SUPPORTED;
+
+    hipStream_t s = (hipStream_t)stream;
+    if (pk::launch_wino_filter(f, U, Cin, Cout, s) != hipSuccess) return PK_ERR_LAUNCH;
+    if (pk::launch_wino_input(x, V, H, W, Cin, pt, pl, w.TH, w.TW, w.T, in4, s) != hipSuccess) return PK_ERR_LAUNCH;
+    KernelArgs a;
+    memset(&a, 0, sizeof(a));
+    a.A = V;
+    a.B = U;
+    a.C = Mm;
+    a.lda = Cin;
+    a.ldb = Cout;
+    a.ldc = Cout;
+    a.alpha = 1.f;
+    a.beta = 0.f;
+    a.nbatch = 16;
+    a.stride_a = w.T * Cin;
+    a.stride_b = Cin * Cout;
+    a.stride_c = w.T * Cout;
+    fill_common(a, c, w.T, Cout, Cin, 1);
+    if (c->launch(a, s) != hipSuccess) return PK_ERR_LAUNCH;
+    if (pk::launch_wino_output(Mm, y, Ho, Wo, Cout, w.TH, w.TW, w.T, out4, s) != hipSuccess) return PK_ERR_LAUNCH;
+    t_last_config = c->name;
+    return PK_OK;
+}
+
+}  // extern "C"

@@ -20,6 +20,11 @@ struct KernelArgs {
     // with m = (n*Ho + ho)*Wo + wo and k = (kh*KW + kw)*Cin + ci.
     int H, W, Cin, KW, sh, sw, pt, pl, Ho, Wo;
     int KH, batch;  // used by the direct convolution only
+    // batched products (non-persistent GEMM instances): grid.y = nbatch
+    // independent products, matrix b at A + b*stride_a, B + b*stride_b,
+    // C + b*stride_c (elements).  0 = one product.
+    int nbatch;
+    int64_t stride_a, stride_b, stride_c;
 };
 
 }  // namespace pk

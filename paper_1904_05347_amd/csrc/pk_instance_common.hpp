@@ -10,7 +10,7 @@ namespace pk {
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
 static hipError_t launch_gemm(const KernelArgs &a, hipStream_t stream)
 {
-    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), 1u, (unsigned)a.splits);
+    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
     const dim3 block(64 * WAVES_M * WAVES_N);
     hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC>),
                        grid, block, 0, stream, a);

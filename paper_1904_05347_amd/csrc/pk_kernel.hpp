@@ -426,6 +426,12 @@ gemm_kernel(KernelArgs p)
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int l32 = lane & 31, h = lane >> 5;
 
+    if constexpr (AMODE != A_CONV) {  // product blockIdx.y of a batch
+        const int64_t bz = blockIdx.y;
+        p.A += bz * p.stride_a;
+        p.B += bz * p.stride_b;
+        p.C += bz * p.stride_c;
+    }
     int tm, tn;
     tile_coords(p, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;

@@ -116,6 +116,45 @@ def test_conv_argument_checks(pk):
     assert binding.conv2d_fwd_raw(*[args[k] for k in order]) == 0
 
 
+def test_winograd_argument_checks(pk):
+    """Host-side checks of pk_conv2d_winograd_fwd: the positions of
+    pk_conv2d_fwd, then the window / stride it supports and its workspace."""
+    from paper_1904_05347_amd import binding
+    fake = 0x10000
+    N, H, W, Cin, Cout = 2, 5, 7, 6, 10
+    need = pk.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, 1, 1, 1, 1)
+    # U (16 Cin Cout), V (16 T Cin), M (16 T Cout) floats, T = N ceil(Ho/2) ceil(Wo/2)
+    T = N * 3 * 4
+    floor = 4 * 16 * (Cin * Cout + T * Cin + T * Cout)
+    assert floor <= need < floor + 3 * 256, (need, floor)
+    ws = fake + (8 << 20)
+    good = dict(x=fake, N=N, H=H, W=W, Cin=Cin, f=fake + (1 << 20), KH=3, KW=3, Cout=Cout, sh=1, sw=1,
+                pt=1, pl=1, pb=1, pr=1, y=fake + (2 << 20), Ho=5, Wo=7, ws=ws, ws_bytes=need)
+    order = list(good)
+
+    def call(**kw):
+        args = dict(good, **kw)
+        return binding.conv2d_winograd_raw(*[args[k] for k in order])
+
+    bad = [("N", -1, 2), ("H", 0, 3), ("W", 0, 4), ("Cin", 0, 5), ("KH", 0, 7), ("KW", 0, 8),
+           ("Cout", 0, 9), ("sh", 0, 10), ("sw", 0, 11), ("pt", -1, 12), ("pl", -1, 13),
+           ("pb", -1, 14), ("pr", -1, 15), ("Ho", 4, 17), ("Wo", 6, 18),
+           ("x", None, 1), ("f", None, 6), ("y", None, 16), ("y", fake + 64, 16)]
+    for key, val, pos in bad:
+        st = call(**{key: val})
+        assert (st, pk.last_invalid_param()) == (1, pos), (key, val, st, pk.last_invalid_param())
+    # windows and strides other than 3 x 3, stride 1
+    assert call(KH=5, KW=5, pt=2, pl=2, pb=2, pr=2) == 2
+    assert call(KH=1, KW=1, pt=0, pl=0, pb=0, pr=0) == 2
+    assert call(sh=2, sw=2, Ho=3, Wo=4) == 2
+    # the workspace is required, large enough, aligned and disjoint from the tensors
+    assert call(ws=None) == 3
+    assert call(ws_bytes=need - 1) == 3
+    assert (call(ws=ws + 4), pk.last_invalid_param()) == (1, 19)
+    assert (call(ws=fake + (1 << 20) - 64), pk.last_invalid_param()) == (1, 19)
+    assert call(N=0) == 0
+
+
 def test_config_space(pk):
     cfgs = pk.configs()
     assert len(cfgs) >= 10
