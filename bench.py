@@ -41,11 +41,12 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
-    ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep", "winograd"),
+    ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep", "winograd", "ablations"),
                     help="step: the benchmark step (default); layers: every VGG-16 / ResNet-50 layer of the "
                          "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
                          "the vendor fp32 GEMM beside it; winograd: the 3x3 stride-1 layers through the "
-                         "Winograd F(2x2, 3x3) path beside the default path")
+                         "Winograd F(2x2, 3x3) path beside the default path; ablations: double buffering, "
+                         "vector width, wave-tile shape, tile size vs CU fill, warm vs cold caches")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
                          "the HBM copy bandwidth and the vendor fp32 GEMM at 4096^3, print one JSON line")
@@ -178,7 +179,45 @@ def cpu_baseline(oracle, host, ops, seconds, np):
         "kind": "oracle",
         "sample": "%d outputs drawn uniformly from every op of one step (fraction %.3g of each op's "
                   "outputs, %.2f GFLOP nominal, fp64 accumulation), %.1f s" % (n_out, frac, flops / 1e9, t),
+        "cpu_model": _cpu_model(),
+        "per_core": per_core_baseline(oracle, np),
     }
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def per_core_baseline(oracle, np):
+    """The oracle on one thread: the whole 512^3 GEMM and the whole batch-1
+    56x56x64 -> 64 3x3 convolution (the two small parity workloads), GFLOP/s."""
+    from paper_1904_05347_amd import workloads as wl
+    threads = oracle.num_threads()
+    oracle.set_threads(1)
+    try:
+        g = wl.GEMM_SMALL
+        A, B, C = g.inputs()
+        t0 = time.perf_counter()
+        oracle.sgemm(g.trans_a, g.trans_b, g.M, g.N, g.K, g.alpha, A, g.lda, B, g.ldb, g.beta, C, g.ldc)
+        tg = time.perf_counter() - t0
+        c = wl.CONV_SMALL
+        x, f = c.inputs()
+        t0 = time.perf_counter()
+        oracle.conv2d(x, f, c.stride, c.pads)
+        tc = time.perf_counter() - t0
+        Ho, Wo = c.out_hw
+    finally:
+        oracle.set_threads(threads)
+    return {"threads": 1,
+            "gemm_512_gflops": round(g.flops / tg / 1e9, 3),
+            "conv_b1_56x56x64_gflops": round(wl.conv_flops(c, Ho, Wo) / tc / 1e9, 3)}
 
 
 def _time_ms(torch, fn, min_ms=20.0):
@@ -271,6 +310,106 @@ def run_winograd_suite(torch, pk, wl):
     return {"suite": "winograd", "dtype": "f32", "data": "synthetic", "rows": rows}
 
 
+def _time_each(torch, fn, iters=50, between=None):
+    """Median and minimum (ms) of `iters` individually timed calls, each
+    bracketed by HIP events on the current stream; `between` runs untimed
+    before each call (e.g. a scratch write that evicts the caches)."""
+    fn()
+    fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    times = []
+    for _ in range(iters):
+        if between is not None:
+            between()
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    times.sort()
+    return times[len(times) // 2], times[0]
+
+
+def run_ablations(torch, pk, wl):
+    """The design choices the paper varies, measured on MI355X: double
+    buffering (two LDS stages vs one), load vector width (16/8/4 bytes),
+    square vs elongated wave tiles at equal accumulator count, tile size
+    against CU fill, and warm vs cold caches for the layers whose working set
+    fits the 256 MB last-level cache.  Median and min of 50 individually
+    timed calls each."""
+    rows = []
+
+    def gemm_rows(ablation, case, variants):
+        A, B, C = case.inputs()
+        dA, dB, dC = (torch.from_numpy(v).cuda() for v in (A, B, C))
+        for label, cfg in variants:
+            pk.force_config(cfg)
+            try:
+                med, mn = _time_each(torch, lambda: pk.gemm(dA, dB, dC, alpha=case.alpha, beta=case.beta))
+                used = pk.last_config_name()
+            finally:
+                pk.force_config(None)
+            c = next(x for x in pk.configs() if x["name"] == cfg)
+            tiles = -(-case.M // c["bm"]) * -(-case.N // c["bn"])
+            rows.append({"ablation": ablation, "shape": case.name, "variant": label, "config": used,
+                         "ms_median": round(med, 4), "ms_min": round(mn, 4),
+                         "tflops": round(case.flops / (med * 1e-3) / 1e12, 2), "tiles": tiles,
+                         "tiles_per_cu": round(tiles / 256, 2)})
+            print("bench: %s %s %s %.4f ms" % (ablation, case.name, label, med), file=sys.stderr, flush=True)
+        del dA, dB, dC
+
+    g1024, g2048, g4096 = wl.GEMM_SWEEP[0], wl.GEMM_SWEEP[1], wl.GEMM_SWEEP[2]
+    for case in (g4096, g1024):
+        gemm_rows("double buffering", case, [
+            ("two LDS stages 128x128x16", "gemm_128x128x16_w2x2_nn_v44"),
+            ("one LDS stage 128x128x16", "gemm_128x128x16_w2x2_nn_v44_s1"),
+            ("two LDS stages 64x64x32", "gemm_64x64x32_w2x2_nn_v44"),
+            ("one LDS stage 64x64x32", "gemm_64x64x32_w2x2_nn_v44_s1"),
+            ("two LDS stages 256x256x32", "gemm_256x256x32_w2x4_nn_v44_o2"),
+            ("one LDS stage 256x256x32", "gemm_256x256x32_w2x4_nn_v44_o2_s1")])
+        gemm_rows("vector width", case, [
+            ("16-byte loads", "gemm_128x128x16_w2x2_nn_v44"),
+            ("8-byte loads", "gemm_128x128x16_w2x2_nn_v22"),
+            ("4-byte loads", "gemm_128x128x16_w2x2_nn_v11")])
+        gemm_rows("wave tile shape", case, [
+            ("64x64 per wave (square)", "gemm_128x128x16_w2x2_nn_v44"),
+            ("32x128 per wave", "gemm_128x128x16_w4x1_nn_v44"),
+            ("128x32 per wave", "gemm_128x128x16_w1x4_nn_v44")])
+    for case in (g1024, g2048, g4096):
+        gemm_rows("tile size vs CU fill", case, [
+            ("64x64 tiles", "gemm_64x64x32_w2x2_nn_v44"),
+            ("128x128 tiles", "gemm_128x128x32_w2x2_nn_v44"),
+            ("256x256 tiles", "gemm_256x256x32_w2x4_nn_v44_o2"),
+            ("128x128 tiles, persistent", "gemm_128x128x32_w2x4_nn_v44_o2_p")])
+
+    # warm vs cold: a 512 MiB scratch write between calls evicts L2 and MALL
+    scratch = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+    by_name = {c.name: c for c in wl.STEP_CONVS}
+    for name in ("vgg16 conv1_1 b32 224x224x3->64 3x3", "resnet50 b32 56x56x64->64 1x1",
+                 "resnet50 b32 56x56x64->256 1x1"):
+        case = by_name[name]
+        x, f = case.inputs()
+        N, H, W, Cin = case.x_shape
+        KH, KW, _, Cout = case.f_shape
+        Ho, Wo = case.out_hw
+        dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+        dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+        nbytes = 4 * (x.size + f.size + dy.numel())
+
+        def run():
+            pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads, out=dy)
+
+        for label, between in (("warm", None), ("cold (512 MiB write between calls)", lambda: scratch.fill_(1.0))):
+            med, mn = _time_each(torch, run, between=between)
+            rows.append({"ablation": "cache state", "shape": name, "variant": label, "config": pk.last_config_name(),
+                         "ms_median": round(med, 4), "ms_min": round(mn, 4),
+                         "tflops": round(wl.conv_flops(case, Ho, Wo) / (med * 1e-3) / 1e12, 2),
+                         "gbs": round(nbytes / (med * 1e-3) / 1e9, 1)})
+            print("bench: cache %s %s %.4f ms" % (name, label, med), file=sys.stderr, flush=True)
+        del dx, df, dy
+    return {"suite": "ablations", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
 def run_gemm_sweep(torch, pk, wl):
     """The paper's GEMM sweep (M, N, K powers of two in [64, 1024]), with the
     vendor fp32 GEMM (torch.matmul, tf32 off) timed beside it as context."""
@@ -349,6 +488,9 @@ def main():
     if args.suite == "winograd":
         print(json.dumps(run_winograd_suite(torch, pk, wl)))
         return
+    if args.suite == "ablations":
+        print(json.dumps(run_ablations(torch, pk, wl)))
+        return
     print("bench: generating inputs", file=sys.stderr, flush=True)
     ops, host = make_ops(torch, pk, wl)
     stream = torch.cuda.current_stream()
@@ -388,12 +530,20 @@ def main():
     step_flops = sum(op.flops for op in ops)
     value = step_flops / (ms_per_step * 1e-3) / 1e9
 
+    # the denominators this GPU sustains, measured after the timed region
+    from paper_1904_05347_amd import binding
+    measured = {"mfma_random_operands_tflops": round(binding.probe_mfma_data_tflops(768, 2000), 2),
+                "copy_gbs": round(binding.probe_copy_gbs(1024), 1)}
+
     per_op = []
     for i, op in enumerate(ops):
-        ms = sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(args.steps)) / args.steps
+        each = sorted(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(args.steps))
+        ms = sum(each) / args.steps
         tflops = op.flops / (ms * 1e-3) / 1e12
         per_op.append({"op": op.name, "config": op.config, "ms": round(ms, 4),
+                       "ms_median": round(each[len(each) // 2], 4), "ms_min": round(each[0], 4),
                        "tflops": round(tflops, 2), "frac_mfma_peak": round(tflops / FP32_MFMA_PEAK_TFLOPS, 4),
+                       "frac_measured_mfma": round(tflops / measured["mfma_random_operands_tflops"], 4),
                        "gbs": round(op.bytes / (ms * 1e-3) / 1e9, 1)})
     dom = max(range(len(ops)), key=lambda i: per_op[i]["ms"])
     d = per_op[dom]
@@ -427,6 +577,7 @@ def main():
                    "frac_mfma_peak": round(value / 1e3 / FP32_MFMA_PEAK_TFLOPS, 4),
                    "step_gflop": round(step_flops / 1e9, 3)},
         "roofline": roofline,
+        "measured_peaks": measured,
         "cpu_baseline": cpu,
         "per_op": per_op,
     }

@@ -29,6 +29,7 @@ struct Config {
     int persistent; // 1 = grid sized to the resident work-groups, each looping over tiles
     int lds_bytes;
     LaunchFn launch;
+    int single_stage;  // 1 = one LDS stage (no double buffering; an ablation form)
 };
 
 // The registry (defined with the kernel instances, host side only).

@@ -39,6 +39,7 @@
 
 namespace pk {
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
@@ -82,6 +83,13 @@ struct Vec<1> {
     static __device__ __forceinline__ T zero() { return 0.f; }
     static __device__ __forceinline__ T load(const float *p) { return *p; }
     static __device__ __forceinline__ void store(float *p, T v) { *p = v; }
+};
+template <>
+struct Vec<2> {
+    typedef f32x2 T;
+    static __device__ __forceinline__ T zero() { return f32x2{0.f, 0.f}; }
+    static __device__ __forceinline__ T load(const float *p) { return *reinterpret_cast<const f32x2 *>(p); }
+    static __device__ __forceinline__ void store(float *p, T v) { *reinterpret_cast<f32x2 *>(p) = v; }
 };
 template <>
 struct Vec<4> {
@@ -508,6 +516,78 @@ gemm_kernel(KernelArgs p)
         __builtin_amdgcn_sched_barrier(0);
         G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
         stage ^= 1;
+    }
+
+    G::store(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+}
+
+// The same contraction with ONE LDS stage: every K-block is loaded, stored
+// to LDS and multiplied in turn, with a barrier before the store (the last
+// block's reads are done) and one after it.  Nothing overlaps the global
+// loads inside a work-group; only other resident work-groups hide them.  It
+// exists to measure what double buffering (the two-stage pipeline above,
+// Section 3.1.2) buys on this hardware.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_single_stage_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
+    typedef typename G::ALoader ALoader;
+    typedef typename G::BLoader BLoader;
+
+    __shared__ __attribute__((aligned(16))) float smem[G::A_STAGE + G::B_STAGE];
+    float *As = smem;
+    float *Bs = smem + G::A_STAGE;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+
+    if constexpr (AMODE != A_CONV) {
+        const int64_t bz = blockIdx.y;
+        p.A += bz * p.stride_a;
+        p.B += bz * p.stride_b;
+        p.C += bz * p.stride_c;
+    }
+    int tm, tn;
+    tile_coords(p, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    int kbeg, kend;
+    split_range(p, BK, blockIdx.z, kbeg, kend);
+
+    ALoader la;
+    BLoader lb;
+    if constexpr (AMODE == A_CONV)
+        la.init(p, m0, kbeg, tid);
+    else
+        la.init(p.A, p.lda, m0, p.M, kbeg, tid);
+    lb.init(p.B, p.ldb, n0, p.N, kbeg, tid);
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename ALoader::VT ra[ALoader::LOADS];
+    typename BLoader::VT rb[BLoader::LOADS];
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    typename G::FragA fa;
+    typename G::FragB fb;
+
+    for (int kb = kbeg; kb < kend; ++kb) {
+        la.load(ra, kb * BK, p.K);
+        lb.load(rb, kb * BK, p.K);
+        la.advance();
+        lb.advance();
+        __syncthreads();  // the previous block's LDS reads are done
+        la.template store<G::LDA_S>(As, ra, tid);
+        lb.template store<G::LDB_S>(Bs, rb, tid);
+        __syncthreads();
+#pragma unroll
+        for (int g = 0; g < G::NG; ++g) {
+            G::read_group(As, Bs, a_row, b_row, h, g, fa, fb);
+            G::mma_group(acc, fa, fb);
+        }
     }
 
     G::store(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);

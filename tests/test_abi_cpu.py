@@ -167,12 +167,13 @@ def test_config_space(pk):
             continue
         assert c["bm"] % (32 * c["waves_m"]) == 0 and c["bn"] % (32 * c["waves_n"]) == 0
         assert c["bk"] % 8 == 0
-        assert c["stages"] == 2
-        # two LDS stages of the A and B tiles, each row padded by 4 floats
+        assert c["stages"] in (1, 2)
+        assert c["stages"] == 2 or (c["kind"] == 0 and c["name"].endswith("_s1"))
+        # one or two LDS stages of the A and B tiles, each row padded by 4 floats
         a_k = c["kind"] == 1 or not c["trans_a"]
         a_tile = c["bm"] * (c["bk"] + 4) if a_k else c["bk"] * (c["bm"] + 4)
         b_tile = c["bn"] * (c["bk"] + 4) if c["trans_b"] else c["bk"] * (c["bn"] + 4)
-        assert c["lds_bytes"] == 2 * 4 * (a_tile + b_tile), c["name"]
+        assert c["lds_bytes"] == c["stages"] * 4 * (a_tile + b_tile), c["name"]
         assert c["lds_bytes"] <= 160 * 1024
     # every GEMM layout has a 16-byte and a scalar-load instance
     for ta in (0, 1):
