@@ -157,6 +157,45 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
                            float *y, int64_t Ho, int64_t Wo,
                            void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Automated parameter search: the measured, per-device choice of a compiled
+ * configuration that the paper makes by hand for each of its devices
+ * (Section 5) and plans to automate (Section 7).  Every compiled
+ * configuration that takes the problem -- and for the convolution every
+ * split of the reduction from 1 to 8 that the workspace allows -- is run
+ * `iters` times after one untimed call on the caller's operands, on
+ * `stream`, timed with HIP events; the fastest is recorded in a process-wide
+ * table that later calls with the same key consult before the built-in
+ * choices:
+ *   GEMM: (transA, transB, M, N, K);
+ *   convolution: (N*Ho*Wo, Cout, KH*KW*Cin, window, stride), KH == KW and
+ *   sh == sw only (else PK_ERR_NOT_SUPPORTED after validation).
+ * The call synchronizes the stream.  C (y) is written many times: with
+ * beta != 0 its final contents are unspecified, so pass a scratch C.
+ * Arguments and error positions are those of pk_sgemm / pk_conv2d_fwd, then
+ * iters (>= 1), stream, result (non-NULL).  An empty problem records
+ * nothing (result->config is "").  The table holds 256 entries (else
+ * PK_ERR_NOT_SUPPORTED); pk_tune_reset() empties it.
+ */
+typedef struct {
+    char config[64];   /* fastest configuration's name */
+    int splits;        /* split of the reduction it ran with (1 = none) */
+    float ms;          /* its mean time per call */
+    int candidates;    /* (configuration, split) pairs timed */
+} pk_tune_result;
+
+int pk_tune_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K,
+                  float alpha, const float *A, int64_t lda, const float *B, int64_t ldb,
+                  float beta, float *C, int64_t ldc, int iters, void *stream,
+                  pk_tune_result *result);
+int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                       const float *f, int64_t KH, int64_t KW, int64_t Cout,
+                       int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb, int64_t pr,
+                       float *y, int64_t Ho, int64_t Wo,
+                       void *workspace, size_t workspace_bytes,
+                       int iters, void *stream, pk_tune_result *result);
+int pk_tune_reset(void);
+
 /* Static text for a status code. */
 const char *pk_status_string(int status);
 

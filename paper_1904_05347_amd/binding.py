@@ -49,6 +49,11 @@ class ConfigInfo(ctypes.Structure):
                 ("persistent", ctypes.c_int)]
 
 
+class TuneResult(ctypes.Structure):
+    _fields_ = [("config", ctypes.c_char * 64), ("splits", ctypes.c_int), ("ms", ctypes.c_float),
+                ("candidates", ctypes.c_int)]
+
+
 # Every symbol include/pk.h declares, with its ctypes signature.
 SIGNATURES = {
     "pk_sgemm": (ctypes.c_int, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64, ctypes.c_float, _p, _i64,
@@ -63,6 +68,13 @@ SIGNATURES = {
     "pk_conv2d_winograd_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
                                               _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
                                               _p, ctypes.c_size_t, _p]),
+    "pk_tune_sgemm": (ctypes.c_int, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64, ctypes.c_float, _p, _i64,
+                                     _p, _i64, ctypes.c_float, _p, _i64, ctypes.c_int, _p,
+                                     ctypes.POINTER(TuneResult)]),
+    "pk_tune_conv2d_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
+                                          _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
+                                          _p, ctypes.c_size_t, ctypes.c_int, _p, ctypes.POINTER(TuneResult)]),
+    "pk_tune_reset": (ctypes.c_int, []),
     "pk_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "pk_last_invalid_param": (ctypes.c_int, []),
     "pk_last_config_name": (ctypes.c_char_p, []),
@@ -362,3 +374,55 @@ def conv2d_winograd(x, w, padding="SAME", out=None, workspace=None):
                              workspace.numel() * 4, _stream_handle(out))
     _check(st, "pk_conv2d_winograd_fwd")
     return out
+
+
+def _tune_dict(r):
+    return {"config": r.config.decode(), "splits": r.splits, "ms": r.ms, "candidates": r.candidates}
+
+
+def tune_gemm(a, b, c, alpha=1.0, beta=0.0, trans_a=False, trans_b=False, iters=5):
+    """Time every compiled configuration on these operands and record the
+    fastest for this shape (see pk_tune_sgemm).  c is overwritten."""
+    _check_f32_cuda(a, "a")
+    _check_f32_cuda(b, "b")
+    _check_f32_cuda(c, "c")
+    lda, ldb, ldc = _ld_2d(a, "a"), _ld_2d(b, "b"), _ld_2d(c, "c")
+    M, K = (a.size(1), a.size(0)) if trans_a else (a.size(0), a.size(1))
+    Kb, N = (b.size(1), b.size(0)) if trans_b else (b.size(0), b.size(1))
+    if Kb != K or tuple(c.shape) != (M, N):
+        raise ValueError("operand shapes do not match")
+    r = TuneResult()
+    st = load().pk_tune_sgemm(b"T" if trans_a else b"N", b"T" if trans_b else b"N", M, N, K, float(alpha),
+                              a.data_ptr(), lda, b.data_ptr(), ldb, float(beta), c.data_ptr(), ldc, int(iters),
+                              _stream_handle(c), ctypes.byref(r))
+    _check(st, "pk_tune_sgemm")
+    return _tune_dict(r)
+
+
+def tune_conv2d(x, w, stride=(1, 1), padding="SAME", out=None, workspace=None, iters=5):
+    """Time every compiled configuration (and reduction split the workspace
+    allows) on this convolution and record the fastest (see pk_tune_conv2d_fwd)."""
+    import torch
+    _check_f32_cuda(x, "x")
+    _check_f32_cuda(w, "w")
+    N, H, W, Cin = x.shape
+    KH, KW, _, Cout = w.shape
+    sh, sw = (stride, stride) if isinstance(stride, int) else tuple(stride)
+    pt, pl, pb, pr = resolve_padding(padding, H, W, KH, KW, sh, sw)
+    Ho, Wo = conv2d_out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr)
+    if out is None:
+        out = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device=x.device)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        _check_f32_cuda(workspace, "workspace")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * 4
+    r = TuneResult()
+    st = load().pk_tune_conv2d_fwd(x.data_ptr(), N, H, W, Cin, w.data_ptr(), KH, KW, Cout, sh, sw, pt, pl, pb, pr,
+                                   out.data_ptr(), Ho, Wo, ws_ptr, ws_bytes, int(iters), _stream_handle(out),
+                                   ctypes.byref(r))
+    _check(st, "pk_tune_conv2d_fwd")
+    return _tune_dict(r)
+
+
+def tune_reset():
+    _check(load().pk_tune_reset(), "pk_tune_reset")

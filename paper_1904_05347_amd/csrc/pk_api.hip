@@ -169,13 +169,52 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 1},
 };
 
-const TunedShape *find_tuned(int kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t kh, int64_t stride)
+// Entries recorded at run time by pk_tune_sgemm / pk_tune_conv2d_fwd; they
+// take precedence over the built-in table.  Process-wide, under a mutex.
+constexpr int kMaxRuntimeTuned = 256;
+std::mutex g_tuned_mu;
+TunedShape g_tuned[kMaxRuntimeTuned];
+int g_tuned_n = 0;
+
+bool same_key(const TunedShape &t, int kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t kh,
+              int64_t stride)
 {
+    return t.kind == kind && t.ta == ta && t.tb == tb && t.M == M && t.N == N && t.K == K &&
+           (kind == 0 || (t.kh == kh && t.stride == stride));
+}
+
+// The tuned configuration for this key, if any: *out is a copy.
+bool find_tuned(int kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t kh, int64_t stride,
+                TunedShape *out)
+{
+    {
+        std::lock_guard<std::mutex> lock(g_tuned_mu);
+        for (int i = g_tuned_n - 1; i >= 0; --i)
+            if (same_key(g_tuned[i], kind, ta, tb, M, N, K, kh, stride)) {
+                *out = g_tuned[i];
+                return true;
+            }
+    }
     for (const TunedShape &t : kTuned)
-        if (t.kind == kind && t.ta == ta && t.tb == tb && t.M == M && t.N == N && t.K == K &&
-            (kind == 0 || (t.kh == kh && t.stride == stride)))
-            return &t;
-    return nullptr;
+        if (same_key(t, kind, ta, tb, M, N, K, kh, stride)) {
+            *out = t;
+            return true;
+        }
+    return false;
+}
+
+// Records (or replaces) a runtime entry; false when the table is full.
+bool record_tuned(const TunedShape &t)
+{
+    std::lock_guard<std::mutex> lock(g_tuned_mu);
+    for (int i = 0; i < g_tuned_n; ++i)
+        if (same_key(g_tuned[i], t.kind, t.ta, t.tb, t.M, t.N, t.K, t.kh, t.stride)) {
+            g_tuned[i] = t;
+            return true;
+        }
+    if (g_tuned_n == kMaxRuntimeTuned) return false;
+    g_tuned[g_tuned_n++] = t;
+    return true;
 }
 
 // Shapes outside the table, from the same measurements:
@@ -446,8 +485,10 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float al
     if (c) {
         if (!gemm_config_fits(c, ta, tb, vec_ok)) return PK_ERR_NOT_SUPPORTED;
     } else {
-        const TunedShape *t = vec_ok ? find_tuned(0, ta, tb, M, N, K, 0, 0) : nullptr;
+        TunedShape tbuf;
+        const TunedShape *t = find_tuned(0, ta, tb, M, N, K, 0, 0, &tbuf) ? &tbuf : nullptr;
         c = t ? find_config(t->config) : nullptr;
+        if (c && !gemm_config_fits(c, ta, tb, vec_ok)) c = nullptr;
         if (!c) c = select_gemm(ta, tb, M, N, K, vec_ok);
         if (!c) return PK_ERR_NOT_SUPPORTED;
     }
@@ -481,9 +522,13 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
     if (M < 0 || K < 0 || M > kMaxDim || K > kMaxDim || Cout > kMaxDim) return 0;
     // the selector's choice for 16-byte aligned tensors (what the allocator gives)
     const bool v4 = Cin % 4 == 0 && Cout % 4 == 0;
-    if (!gemm_path && pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535) return 0;
-    const TunedShape *tuned = (KH == KW && sh == sw) ? find_tuned(1, 0, 0, M, Cout, K, KH, sh) : nullptr;
+    TunedShape tbuf;
+    const TunedShape *tuned =
+        (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
+    const bool direct_ok = !gemm_path && pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535;
+    if (direct_ok && !(tuned && v4)) return 0;
     const Config *c = (tuned && v4) ? find_config(tuned->config) : nullptr;
+    if (c && c->kind == pk::KIND_DIRECT) return 0;
     if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
     if (!c) return 0;
     if (tuned && v4 && tuned->splits > 0 && t_forced_splits == 0)
@@ -555,7 +600,9 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
 
     const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
-    const TunedShape *tuned = (KH == KW && sh == sw) ? find_tuned(1, 0, 0, M, Cout, K, KH, sh) : nullptr;
+    TunedShape tbuf;
+    const TunedShape *tuned =
+        (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
     if (gemm_path) {
         // 1x1, stride 1, no padding: the image is already the M x Cin matrix.
         const bool vec_ok = gemm_vec_ok(0, 0, M, Cout, Cin, x, Cin, f, Cout);
@@ -573,10 +620,11 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         if (c) {
             if (!conv_config_fits(c, va4, vb4)) return PK_ERR_NOT_SUPPORTED;
             if (c->kind == pk::KIND_DIRECT && !direct_ok) return PK_ERR_NOT_SUPPORTED;
-        } else if (direct_ok) {
-            c = find_config("direct_8x32x64_k32");
         } else {
-            c = (tuned && va4 && vb4) ? find_config(tuned->config) : nullptr;
+            // a measured choice first (it may name the direct kernel), then the rules
+            c = tuned ? find_config(tuned->config) : nullptr;
+            if (c && (!conv_config_fits(c, va4, vb4) || (c->kind == pk::KIND_DIRECT && !direct_ok))) c = nullptr;
+            if (!c && direct_ok) c = find_config("direct_8x32x64_k32");
             if (!c) c = select_conv(M, Cout, va4, vb4);
         }
         if (!c) return PK_ERR_NOT_SUPPORTED;
@@ -776,6 +824,194 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
     if (c->launch(a, s) != hipSuccess) return PK_ERR_LAUNCH;
     if (pk::launch_wino_output(Mm, y, Ho, Wo, Cout, w.TH, w.TW, w.T, out4, s) != hipSuccess) return PK_ERR_LAUNCH;
     t_last_config = c->name;
+    return PK_OK;
+}
+
+
+// ------------------------------------------------------------ tuning
+
+}  // extern "C"
+
+namespace {
+
+struct EventPair {
+    hipEvent_t a = nullptr, b = nullptr;
+    bool ok = false;
+    EventPair() { ok = hipEventCreate(&a) == hipSuccess && hipEventCreate(&b) == hipSuccess; }
+    ~EventPair()
+    {
+        if (a) (void)hipEventDestroy(a);
+        if (b) (void)hipEventDestroy(b);
+    }
+};
+
+// The calling thread's forced configuration and split, restored on exit.
+struct ForceScope {
+    const Config *c0;
+    bool set0;
+    int s0;
+    ForceScope() : c0(t_forced), set0(t_forced_set), s0(t_forced_splits) {}
+    ~ForceScope()
+    {
+        t_forced = c0;
+        t_forced_set = set0;
+        t_forced_splits = s0;
+    }
+    void force(const Config *c, int splits)
+    {
+        t_forced = c;
+        t_forced_set = true;
+        t_forced_splits = splits;
+    }
+};
+
+// Mean milliseconds per call of `call` over `iters` calls after one untimed
+// call; negative with *st set when a call does not return PK_OK.
+template <typename F>
+float time_calls(F call, int iters, hipStream_t s, EventPair &ev, int *st)
+{
+    *st = call();
+    if (*st != PK_OK) return -1.f;
+    if (hipEventRecord(ev.a, s) != hipSuccess) {
+        *st = PK_ERR_LAUNCH;
+        return -1.f;
+    }
+    for (int i = 0; i < iters; ++i) {
+        *st = call();
+        if (*st != PK_OK) return -1.f;
+    }
+    float ms = 0.f;
+    if (hipEventRecord(ev.b, s) != hipSuccess || hipEventSynchronize(ev.b) != hipSuccess ||
+        hipEventElapsedTime(&ms, ev.a, ev.b) != hipSuccess) {
+        *st = PK_ERR_LAUNCH;
+        return -1.f;
+    }
+    return ms / iters;
+}
+
+void fill_result(pk_tune_result *r, const Config *c, int splits, float ms, int candidates)
+{
+    snprintf(r->config, sizeof(r->config), "%s", c ? c->name : "");
+    r->splits = splits;
+    r->ms = ms;
+    r->candidates = candidates;
+}
+
+}  // namespace
+
+extern "C" {
+
+int pk_tune_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
+                  int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, int iters,
+                  void *stream, pk_tune_result *result)
+{
+    begin();
+    if (iters < 1) return invalid(14);
+    if (!result) return invalid(16);
+    fill_result(result, nullptr, 0, 0.f, 0);
+    // validates every argument (positions as for pk_sgemm) and warms up
+    int st = pk_sgemm(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream);
+    if (st != PK_OK) return st;
+    if (M == 0 || N == 0 || K == 0 || alpha == 0.f) return PK_OK;  // no contraction runs
+    const int ta = trans_flag(transA), tb = trans_flag(transB);
+    hipStream_t s = (hipStream_t)stream;
+    EventPair ev;
+    if (!ev.ok) return PK_ERR_LAUNCH;
+    const Config *best = nullptr;
+    float best_ms = 0.f;
+    int timed = 0;
+    {
+        ForceScope scope;
+        int n = 0;
+        const Config *cfgs = pk::configs(&n);
+        for (int i = 0; i < n; ++i) {
+            const Config *c = &cfgs[i];
+            if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb) continue;
+            scope.force(c, 0);
+            const float ms = time_calls(
+                [&] { return pk_sgemm(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream); },
+                iters, s, ev, &st);
+            if (st == PK_ERR_LAUNCH) return st;
+            if (ms < 0.f) continue;  // this configuration does not take these operands
+            ++timed;
+            if (!best || ms < best_ms) {
+                best = c;
+                best_ms = ms;
+            }
+        }
+    }
+    if (!best) return PK_ERR_NOT_SUPPORTED;
+    if (!record_tuned({0, ta, tb, M, N, K, 0, 0, best->name, 0})) return PK_ERR_NOT_SUPPORTED;
+    fill_result(result, best, 1, best_ms, timed);
+    t_last_param = 0;
+    t_last_config = best->name;
+    return PK_OK;
+}
+
+int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, const float *f, int64_t KH,
+                       int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb,
+                       int64_t pr, float *y, int64_t Ho, int64_t Wo, void *workspace, size_t workspace_bytes,
+                       int iters, void *stream, pk_tune_result *result)
+{
+    begin();
+    if (iters < 1) return invalid(21);
+    if (!result) return invalid(23);
+    fill_result(result, nullptr, 0, 0.f, 0);
+    auto call = [&] {
+        return pk_conv2d_fwd(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo, workspace,
+                             workspace_bytes, stream);
+    };
+    int st = call();  // validates every argument (positions as for pk_conv2d_fwd) and warms up
+    if (st != PK_OK) return st;
+    if (N == 0) return PK_OK;
+    if (KH != KW || sh != sw) return PK_ERR_NOT_SUPPORTED;  // the table's key has one window and stride
+    const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
+    const int64_t M = N * Ho * Wo, K = KH * KW * Cin;
+    hipStream_t s = (hipStream_t)stream;
+    EventPair ev;
+    if (!ev.ok) return PK_ERR_LAUNCH;
+    static const int kSplits[] = {1, 2, 3, 4, 6, 8};
+    const Config *best = nullptr;
+    int best_splits = 1;
+    float best_ms = 0.f;
+    int timed = 0;
+    {
+        ForceScope scope;
+        int n = 0;
+        const Config *cfgs = pk::configs(&n);
+        for (int i = 0; i < n; ++i) {
+            const Config *c = &cfgs[i];
+            const bool takes = gemm_path ? (c->kind == pk::KIND_GEMM && !c->trans_a && !c->trans_b)
+                                         : (c->kind == pk::KIND_CONV || c->kind == pk::KIND_DIRECT);
+            if (!takes) continue;
+            for (int sp : kSplits) {
+                if (sp > 1 && (c->kind == pk::KIND_DIRECT || workspace_bytes < (size_t)sp * M * Cout * sizeof(float)))
+                    break;
+                scope.force(c, sp);
+                const float ms = time_calls(call, iters, s, ev, &st);
+                if (st == PK_ERR_LAUNCH) return st;
+                if (ms < 0.f) break;  // this configuration does not take this problem
+                ++timed;
+                if (!best || ms < best_ms) {
+                    best = c;
+                    best_splits = sp;
+                    best_ms = ms;
+                }
+            }
+        }
+    }
+    if (!best) return PK_ERR_NOT_SUPPORTED;
+    if (!record_tuned({1, 0, 0, M, Cout, K, (int)KH, (int)sh, best->name, best_splits})) return PK_ERR_NOT_SUPPORTED;
+    fill_result(result, best, best_splits, best_ms, timed);
+    t_last_param = 0;
+    t_last_config = best->name;
+    return PK_OK;
+}
+
+int pk_tune_reset(void)
+{
+    std::lock_guard<std::mutex> lock(g_tuned_mu);
+    g_tuned_n = 0;
     return PK_OK;
 }
 

@@ -155,6 +155,25 @@ def test_winograd_argument_checks(pk):
     assert call(N=0) == 0
 
 
+def test_tune_argument_checks(pk):
+    """The tuner's own arguments are checked before anything runs."""
+    from paper_1904_05347_amd import binding
+    lib = pk.load()
+    fake = 0x10000
+    r = binding.TuneResult()
+    st = lib.pk_tune_sgemm(b"N", b"N", 8, 8, 8, 1.0, fake, 8, fake + 4096, 8, 0.0, fake + 8192, 8, 0, None,
+                           ctypes.byref(r))
+    assert (st, pk.last_invalid_param()) == (1, 14)
+    st = lib.pk_tune_sgemm(b"N", b"N", 8, 8, 8, 1.0, fake, 8, fake + 4096, 8, 0.0, fake + 8192, 8, 3, None, None)
+    assert (st, pk.last_invalid_param()) == (1, 16)
+    conv = [fake, 1, 5, 5, 4, fake + (1 << 20), 3, 3, 4, 1, 1, 1, 1, 1, 1, fake + (2 << 20), 5, 5, None, 0]
+    st = lib.pk_tune_conv2d_fwd(*conv, 0, None, ctypes.byref(r))
+    assert (st, pk.last_invalid_param()) == (1, 21)
+    st = lib.pk_tune_conv2d_fwd(*conv, 2, None, None)
+    assert (st, pk.last_invalid_param()) == (1, 23)
+    assert lib.pk_tune_reset() == 0
+
+
 def test_config_space(pk):
     cfgs = pk.configs()
     assert len(cfgs) >= 10
