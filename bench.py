@@ -41,12 +41,14 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
-    ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep", "winograd", "ablations"),
+    ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep", "winograd", "ablations",
+                                                      "tune"),
                     help="step: the benchmark step (default); layers: every VGG-16 / ResNet-50 layer of the "
                          "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
                          "the vendor fp32 GEMM beside it; winograd: the 3x3 stride-1 layers through the "
                          "Winograd F(2x2, 3x3) path beside the default path; ablations: double buffering, "
-                         "vector width, wave-tile shape, tile size vs CU fill, warm vs cold caches")
+                         "vector width, wave-tile shape, tile size vs CU fill, warm vs cold caches; tune: "
+                         "the automated parameter search against the built-in choices")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
                          "the HBM copy bandwidth and the vendor fp32 GEMM at 4096^3, print one JSON line")
@@ -60,12 +62,18 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
 
 
 def kernel_source_hash():
-    """Hash of the HIP sources: counters taken on other kernels no longer apply."""
+    """Hash of the HIP sources the benchmark step runs (the contraction and
+    direct kernels, their instances and the selection that picks
+    configuration and split): counters taken on other code no longer apply.
+    The Winograd transforms and the probes are not part of the step."""
     import glob
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1904_05347_amd", "csrc")
+    skip = {"pk_winograd.hip", "pk_probe.hip"}
     for path in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        if os.path.basename(path) in skip:
+            continue
         with open(path, "rb") as fh:
             h.update(os.path.basename(path).encode())
             h.update(fh.read())
@@ -221,9 +229,10 @@ def per_core_baseline(oracle, np):
 
 
 def _time_ms(torch, fn, min_ms=20.0):
-    """Mean duration of fn on the current stream: 2 warm-up calls, then enough
-    calls to span about min_ms."""
-    fn()
+    """Duration of fn on the current stream: after about 10 ms of untimed
+    calls (so the clocks have left any idle state the host-side set-up let
+    them fall into), three runs of back-to-back calls spanning about min_ms
+    each; the median run's mean per call."""
     fn()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -232,13 +241,18 @@ def _time_ms(torch, fn, min_ms=20.0):
     e1.record()
     torch.cuda.synchronize()
     one = max(e0.elapsed_time(e1), 1e-3)
-    iters = int(min(max(min_ms / one, 3), 200))
-    e0.record()
-    for _ in range(iters):
+    for _ in range(int(min(max(10.0 / one, 2), 400))):
         fn()
-    e1.record()
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / iters
+    iters = int(min(max(min_ms / one, 3), 200))
+    runs = []
+    for _ in range(3):
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        runs.append(e0.elapsed_time(e1) / iters)
+    return sorted(runs)[1]
 
 
 def run_layer_suite(torch, pk, wl):
@@ -410,6 +424,63 @@ def run_ablations(torch, pk, wl):
     return {"suite": "ablations", "dtype": "f32", "data": "synthetic", "rows": rows}
 
 
+def run_tune_suite(torch, pk, wl):
+    """The automated parameter search against the built-in choices: for the
+    benchmark step's ops and every layer of the paper's tables at batch 4,
+    the default configuration's time, then pk_tune_* on the same operands,
+    then the recorded choice's time (back-to-back timing as in the layer
+    suite)."""
+    rows = []
+    pk.tune_reset()
+    for case in wl.STEP_GEMMS:
+        A, B, C = case.inputs()
+        dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+        dC = torch.from_numpy(C).cuda()
+        ta, tb = case.trans_a == "T", case.trans_b == "T"
+
+        def run():
+            pk.gemm(dA, dB, dC, alpha=case.alpha, beta=case.beta, trans_a=ta, trans_b=tb)
+
+        ms0 = _time_ms(torch, run)
+        cfg0 = pk.last_config_name()
+        scratch = torch.empty_like(dC)
+        r = pk.tune_gemm(dA, dB, scratch, alpha=case.alpha, beta=case.beta, trans_a=ta, trans_b=tb, iters=5)
+        ms1 = _time_ms(torch, run)
+        rows.append({"op": case.name, "default": cfg0, "default_ms": round(ms0, 4), "tuned": r["config"],
+                     "tuned_splits": r["splits"], "tuned_ms": round(ms1, 4), "candidates": r["candidates"],
+                     "speedup": round(ms0 / ms1, 3)})
+        print("bench: tune %s %s -> %s %.3fx" % (case.name, cfg0, r["config"], ms0 / ms1), file=sys.stderr, flush=True)
+        del dA, dB, dC, scratch
+    for case in list(wl.STEP_CONVS) + list(wl.layer_suite(4)):
+        x, f = case.inputs()
+        N, H, W, Cin = case.x_shape
+        KH, KW, _, Cout = case.f_shape
+        if KH != KW or case.stride[0] != case.stride[1]:
+            continue
+        Ho, Wo = pk.conv2d_out_dims(H, W, KH, KW, *case.stride, *case.pads)
+        dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+        dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+        # room for the default rule's split and for every split the tuner tries
+        wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
+        ws = torch.empty(max(8 * N * Ho * Wo * Cout, wsb // 4), dtype=torch.float32, device="cuda")
+
+        def run():
+            pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads, out=dy, workspace=ws)
+
+        ms0 = _time_ms(torch, run)
+        cfg0 = pk.last_config_name()
+        r = pk.tune_conv2d(dx, df, stride=case.stride, padding=case.pads, out=dy, workspace=ws, iters=3)
+        ms1 = _time_ms(torch, run)
+        rows.append({"op": case.name, "default": cfg0, "default_ms": round(ms0, 4), "tuned": r["config"],
+                     "tuned_splits": r["splits"], "tuned_ms": round(ms1, 4), "candidates": r["candidates"],
+                     "speedup": round(ms0 / ms1, 3)})
+        print("bench: tune %s %s -> %s/%d %.3fx" % (case.name, cfg0, r["config"], r["splits"], ms0 / ms1),
+              file=sys.stderr, flush=True)
+        del dx, df, dy, ws
+    pk.tune_reset()
+    return {"suite": "tune", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
 def run_gemm_sweep(torch, pk, wl):
     """The paper's GEMM sweep (M, N, K powers of two in [64, 1024]), with the
     vendor fp32 GEMM (torch.matmul, tf32 off) timed beside it as context."""
@@ -490,6 +561,9 @@ def main():
         return
     if args.suite == "ablations":
         print(json.dumps(run_ablations(torch, pk, wl)))
+        return
+    if args.suite == "tune":
+        print(json.dumps(run_tune_suite(torch, pk, wl)))
         return
     print("bench: generating inputs", file=sys.stderr, flush=True)
     ops, host = make_ops(torch, pk, wl)

@@ -161,10 +161,12 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
  * Automated parameter search: the measured, per-device choice of a compiled
  * configuration that the paper makes by hand for each of its devices
  * (Section 5) and plans to automate (Section 7).  Every compiled
- * configuration that takes the problem -- and for the convolution every
- * split of the reduction from 1 to 8 that the workspace allows -- is run
- * `iters` times after one untimed call on the caller's operands, on
- * `stream`, timed with HIP events; the fastest is recorded in a process-wide
+ * configuration that takes the problem (the single-LDS-stage ablation forms
+ * excepted) -- and for the convolution every split of the reduction from 1
+ * to 8 that the workspace allows -- runs one untimed call and then three
+ * timed runs of `iters` calls (more for short calls: up to about 1 ms per
+ * run) on the caller's operands, on `stream` (HIP events; the median run
+ * counts); the fastest is recorded in a process-wide
  * table that later calls with the same key consult before the built-in
  * choices:
  *   GEMM: (transA, transB, M, N, K);

@@ -159,13 +159,13 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
     {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
     {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44", 1},
-    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 3},
+    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 6},
     // ResNet-50 bottleneck layers at batch 32
     {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},
     {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x64_w2x4_v44_o2", 1},
     {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
     {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
-    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 4},
+    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 6},
     {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 1},
 };
 
@@ -267,12 +267,17 @@ const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4)
 }
 
 // Split of the K reduction when the output alone gives too few work-groups.
+// Fewer than four rounds of work-groups leave the last round partly idle
+// (wave quantization); long reductions are split until the items fill about
+// four rounds, keeping at least 8 K-blocks per split.  Measured with the
+// automated search on the deep VGG-16 layers at batch 4 (1.13-1.22x) and the
+// 14x14x512 layer at batch 32.
 int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 {
     const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
     const int64_t nkb = ceil_div(K, c->bk);
-    if (tiles >= kCUs) return 1;
-    int64_t s = ceil_div(2 * kCUs, tiles);
+    if (tiles >= 4 * kCUs) return 1;
+    int64_t s = ceil_div(4 * kCUs, tiles);
     const int64_t max_by_k = nkb / 8;  // keep at least 8 K-blocks per split
     if (s > max_by_k) s = max_by_k;
     if (s > 16) s = 16;
@@ -865,28 +870,47 @@ struct ForceScope {
     }
 };
 
-// Mean milliseconds per call of `call` over `iters` calls after one untimed
-// call; negative with *st set when a call does not return PK_OK.
+// Milliseconds per call of `call`: one untimed call, then three timed runs
+// of `iters` back-to-back calls; the median run's mean (one disturbed run
+// does not decide).  Negative with *st set when a call does not return PK_OK.
 template <typename F>
 float time_calls(F call, int iters, hipStream_t s, EventPair &ev, int *st)
 {
-    *st = call();
-    if (*st != PK_OK) return -1.f;
+    // the untimed call, timed once to size the runs: at least `iters` calls
+    // and about 1 ms per run, so launch jitter does not decide for short calls
+    float first = 0.f;
     if (hipEventRecord(ev.a, s) != hipSuccess) {
         *st = PK_ERR_LAUNCH;
         return -1.f;
     }
-    for (int i = 0; i < iters; ++i) {
-        *st = call();
-        if (*st != PK_OK) return -1.f;
-    }
-    float ms = 0.f;
+    *st = call();
+    if (*st != PK_OK) return -1.f;
     if (hipEventRecord(ev.b, s) != hipSuccess || hipEventSynchronize(ev.b) != hipSuccess ||
-        hipEventElapsedTime(&ms, ev.a, ev.b) != hipSuccess) {
+        hipEventElapsedTime(&first, ev.a, ev.b) != hipSuccess) {
         *st = PK_ERR_LAUNCH;
         return -1.f;
     }
-    return ms / iters;
+    if (first > 0.f && (float)iters * first < 1.f) iters = (int)fminf(1.f / first + 1.f, 200.f);
+    float run[3];
+    for (int r = 0; r < 3; ++r) {
+        if (hipEventRecord(ev.a, s) != hipSuccess) {
+            *st = PK_ERR_LAUNCH;
+            return -1.f;
+        }
+        for (int i = 0; i < iters; ++i) {
+            *st = call();
+            if (*st != PK_OK) return -1.f;
+        }
+        float ms = 0.f;
+        if (hipEventRecord(ev.b, s) != hipSuccess || hipEventSynchronize(ev.b) != hipSuccess ||
+            hipEventElapsedTime(&ms, ev.a, ev.b) != hipSuccess) {
+            *st = PK_ERR_LAUNCH;
+            return -1.f;
+        }
+        run[r] = ms / iters;
+    }
+    const float lo = fminf(run[0], fminf(run[1], run[2])), hi = fmaxf(run[0], fmaxf(run[1], run[2]));
+    return run[0] + run[1] + run[2] - lo - hi;
 }
 
 void fill_result(pk_tune_result *r, const Config *c, int splits, float ms, int candidates)
@@ -926,7 +950,7 @@ int pk_tune_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, flo
         const Config *cfgs = pk::configs(&n);
         for (int i = 0; i < n; ++i) {
             const Config *c = &cfgs[i];
-            if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb) continue;
+            if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb || c->single_stage) continue;
             scope.force(c, 0);
             const float ms = time_calls(
                 [&] { return pk_sgemm(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream); },
@@ -981,7 +1005,7 @@ int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t 
         const Config *cfgs = pk::configs(&n);
         for (int i = 0; i < n; ++i) {
             const Config *c = &cfgs[i];
-            const bool takes = gemm_path ? (c->kind == pk::KIND_GEMM && !c->trans_a && !c->trans_b)
+            const bool takes = gemm_path ? (c->kind == pk::KIND_GEMM && !c->trans_a && !c->trans_b && !c->single_stage)
                                          : (c->kind == pk::KIND_CONV || c->kind == pk::KIND_DIRECT);
             if (!takes) continue;
             for (int sp : kSplits) {
