@@ -7,12 +7,28 @@
 #include "pk_kernel.hpp"
 
 namespace pk {
+// Whether a launch needs the epilogue that reads C: beta != 0 on an unsplit
+// product (split partial sums never read C; the reduction applies beta).
+// Convolutions always have beta == 0, so their instances never compile it.
+template <int AMODE>
+static bool reads_c(const KernelArgs &a)
+{
+    return AMODE != A_CONV && a.beta != 0.f && a.splits <= 1;
+}
+
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
 static hipError_t launch_gemm(const KernelArgs &a, hipStream_t stream)
 {
     const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
     const dim3 block(64 * WAVES_M * WAVES_N);
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC>),
+    if constexpr (AMODE != A_CONV) {
+        if (reads_c<AMODE>(a)) {
+            hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, true>),
+                               grid, block, 0, stream, a);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, false>),
                        grid, block, 0, stream, a);
     return hipGetLastError();
 }
@@ -22,16 +38,20 @@ static hipError_t launch_gemm(const KernelArgs &a, hipStream_t stream)
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
 static hipError_t launch_gemm_persistent(const KernelArgs &a, hipStream_t stream)
 {
-    auto kernel = gemm_persistent_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC>;
+    const bool beta = reads_c<AMODE>(a);
+    auto kernel = gemm_persistent_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, false>;
+    if constexpr (AMODE != A_CONV) {
+        if (beta) kernel = gemm_persistent_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, true>;
+    }
     const int threads = 64 * WAVES_M * WAVES_N;
-    static int per_cu = 0;  // resident work-groups per CU (same on every MI355X)
-    if (per_cu == 0) {
+    static int per_cu[2] = {0, 0};  // resident work-groups per CU (same on every MI355X)
+    if (per_cu[beta] == 0) {
         int n = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
-        per_cu = n;
+        per_cu[beta] = n;
     }
     const int64_t items = (int64_t)a.tiles_m * a.tiles_n * a.splits;
-    int64_t grid = (int64_t)per_cu * device_cu_count();
+    int64_t grid = (int64_t)per_cu[beta] * device_cu_count();
     if (grid > items) grid = items;
     if (grid >= a.xcds && a.xcds > 1) grid -= grid % a.xcds;
     hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(threads), 0, stream, a);
@@ -43,7 +63,15 @@ static hipError_t launch_gemm_single_stage(const KernelArgs &a, hipStream_t stre
 {
     const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
     const dim3 block(64 * WAVES_M * WAVES_N);
-    hipLaunchKernelGGL((gemm_single_stage_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC>),
+    if constexpr (AMODE != A_CONV) {
+        if (reads_c<AMODE>(a)) {
+            hipLaunchKernelGGL(
+                (gemm_single_stage_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, true>), grid,
+                block, 0, stream, a);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((gemm_single_stage_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, false>),
                        grid, block, 0, stream, a);
     return hipGetLastError();
 }

@@ -362,9 +362,11 @@ struct GemmTile {
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     }
 
-    // Epilogue of one tile: C = alpha * acc (+ beta * C), or split z's partial
-    // sum alpha * acc into the workspace.  Lane (l32, h) of the wave holds
-    // C(row_base + i*32 + 8*(r/4) + r%4, col_base + j*32) in acc[i][j][r].
+    // Epilogue of one tile: C = alpha * acc (+ beta * C when BETA), or split
+    // z's partial sum alpha * acc into the workspace.  Lane (l32, h) of the
+    // wave holds C(row_base + i*32 + 8*(r/4) + r%4, col_base + j*32) in
+    // acc[i][j][r].  BETA = false never reads C (beta == 0).
+    template <bool BETA>
     static __device__ __forceinline__ void store(const KernelArgs &p, const Acc &acc, int row_base, int col_base,
                                                  int z)
     {
@@ -385,24 +387,62 @@ struct GemmTile {
                 }
             return;
         }
+        if constexpr (!BETA) {
 #pragma unroll
-        for (int i = 0; i < RM; ++i)
+            for (int i = 0; i < RM; ++i)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
-                if (row < p.M) {
+                for (int r = 0; r < 16; ++r) {
+                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                    if (row < p.M) {
+                        float *crow = p.C + (int64_t)row * p.ldc;
+#pragma unroll
+                        for (int j = 0; j < RN; ++j) {
+                            const int col = col_base + j * 32;
+                            if (col < p.N) crow[col] = p.alpha * acc[i][j][r];
+                        }
+                    }
+                }
+        } else {
+            // C = alpha * acc + beta * C.  The C values of one 32-row block are
+            // all loaded, and the block's results computed, before its first
+            // store: the memory counter also counts stores, so a result
+            // computed next to its own store makes every store wait for the
+            // one before it (a load that follows a store to C cannot be moved
+            // above it by the compiler).  Interior lanes skip the bounds tests.
+            const bool interior = row_base + (RM - 1) * 32 + 27 < p.M && col_base + (RN - 1) * 32 < p.N;
+            const float alpha = p.alpha, beta = p.beta;
+#pragma unroll
+            for (int i = 0; i < RM; ++i) {
+                float v[16][RN];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                    const float *crow = p.C + (int64_t)row * p.ldc;
+#pragma unroll
+                    for (int j = 0; j < RN; ++j) {
+                        const int col = col_base + j * 32;
+                        v[r][j] = (interior || (row < p.M && col < p.N)) ? crow[col] : 0.f;
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+#pragma unroll
+                    for (int j = 0; j < RN; ++j) {
+                        v[r][j] = fmaf(beta, v[r][j], alpha * acc[i][j][r]);
+                        asm volatile("" : "+v"(v[r][j]));  // materialise here, before the stores
+                    }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
                     float *crow = p.C + (int64_t)row * p.ldc;
 #pragma unroll
                     for (int j = 0; j < RN; ++j) {
                         const int col = col_base + j * 32;
-                        if (col < p.N) {
-                            float v = p.alpha * acc[i][j][r];
-                            if (p.beta != 0.f) v = fmaf(p.beta, crow[col], v);
-                            crow[col] = v;
-                        }
+                        if (interior || (row < p.M && col < p.N)) crow[col] = v[r][j];
                     }
                 }
             }
+        }
     }
 };
 
@@ -415,8 +455,10 @@ __device__ __forceinline__ void split_range(const KernelArgs &p, int bk, int z, 
 }
 
 // OCC: the waves per SIMD the register allocation must leave room for
-// (1 = no constraint beyond the work-group size).
-template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+// (1 = no constraint beyond the work-group size).  BETA: the epilogue reads
+// C (beta != 0); the beta == 0 form never touches C before writing it and
+// carries none of the registers that reading it takes.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC, bool BETA>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 gemm_kernel(KernelArgs p)
 {
@@ -518,7 +560,7 @@ gemm_kernel(KernelArgs p)
         stage ^= 1;
     }
 
-    G::store(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+    G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
 }
 
 // The same contraction with ONE LDS stage: every K-block is loaded, stored
@@ -527,7 +569,7 @@ gemm_kernel(KernelArgs p)
 // loads inside a work-group; only other resident work-groups hide them.  It
 // exists to measure what double buffering (the two-stage pipeline above,
 // Section 3.1.2) buys on this hardware.
-template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC, bool BETA>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 gemm_single_stage_kernel(KernelArgs p)
 {
@@ -590,7 +632,7 @@ gemm_single_stage_kernel(KernelArgs p)
         }
     }
 
-    G::store(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+    G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
 }
 
 // The items (split z, tile) of a persistent launch: item = z * tiles + tile.
@@ -624,7 +666,7 @@ struct ItemWalk {
 // while the last block of the current one computes, and the epilogue's stores
 // overlap the next item's MFMAs, so short reductions (K of one to a few
 // blocks) no longer pay a load latency per tile.
-template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC, bool BETA>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 gemm_persistent_kernel(KernelArgs p)
 {
@@ -725,7 +767,7 @@ gemm_persistent_kernel(KernelArgs p)
         __builtin_amdgcn_sched_barrier(0);
         G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
         if (last_block) {
-            G::store(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, z);
+            G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, z);
             G::zero(acc);
         }
         if (!more) break;
