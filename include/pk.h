@@ -45,7 +45,7 @@ typedef enum {
     PK_OK = 0,
     PK_ERR_INVALID_VALUE = 1, /* an argument is out of range; see pk_last_invalid_param() */
     PK_ERR_NOT_SUPPORTED = 2, /* a well-formed request this library does not implement */
-    PK_ERR_WORKSPACE = 3,     /* a forced split-K configuration lacks workspace */
+    PK_ERR_WORKSPACE = 3,     /* a forced split-K or stream-K configuration lacks workspace */
     PK_ERR_LAUNCH = 4         /* the HIP runtime refused a kernel launch */
 } pk_status;
 
@@ -93,8 +93,12 @@ int pk_conv2d_same_pads(int64_t H, int64_t W, int64_t KH, int64_t KW,
 
 /*
  * Bytes of device workspace that lets pk_conv2d_fwd split the reduction
- * (KH * KW * Cin) of this problem across work-groups; 0 when the chosen
- * configuration needs none.  Host-only.
+ * (KH * KW * Cin) of this problem across work-groups, for the configuration
+ * the next pk_conv2d_fwd call on this thread would choose (a forced one
+ * included); 0 when that configuration needs none.  A split-K configuration
+ * keeps one partial sum of y per slice of the reduction; a stream-K one keeps
+ * two partial tiles per resident work-group and one arrival counter per tile
+ * of y.  Host-only apart from an occupancy query of the kernel.
  */
 size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin,
                                  int64_t KH, int64_t KW, int64_t Cout,
@@ -113,10 +117,14 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin,
  *   sh, sw       strides >= 1.  pt, pl, pb, pr: zero padding >= 0.
  *   y            N x Ho x Wo x Cout, contiguous (NHWC).  Ho, Wo must equal
  *                pk_conv2d_out_dims() of the geometry (else INVALID_VALUE).
- *   workspace    optional device buffer of workspace_bytes; with at least
- *                pk_conv2d_workspace_bytes() the reduction may be split for
- *                small outputs.  NULL / too small selects an unsplit
- *                configuration.  Contents on return are unspecified.
+ *   workspace    optional device buffer of workspace_bytes, 16-byte aligned;
+ *                with at least pk_conv2d_workspace_bytes() the reduction may
+ *                be split across work-groups (split-K, or stream-K: equal
+ *                shares of the (tile, K-block) iterations per resident
+ *                work-group, partial tiles finished by their last
+ *                contributor).  NULL / too small selects a configuration
+ *                that needs none.  Contents on return are unspecified.  Two
+ *                calls that overlap in time must not share a workspace.
  * N == 0 does nothing.  Dilation, groups, bias and activation are not part
  * of this operation.
  */
@@ -226,6 +234,10 @@ typedef struct {
     int lds_bytes;   /* LDS per work-group */
     int occupancy;   /* waves per SIMD its registers are allotted for (1 = unconstrained) */
     int persistent;  /* 1 = one work-group per resident slot, each looping over tiles */
+    int streamk;     /* 1 = stream-K: resident work-groups share the (tile, K-block) iterations
+                        evenly; convolution calls only (it needs the workspace) */
+    int bres;        /* 1 = op(B) held whole in LDS while row tiles of A stream past; runs
+                        only products with K == bk and N == bn (op(A) = A, op(B) = B) */
 } pk_config_info;
 
 int pk_num_configs(void);

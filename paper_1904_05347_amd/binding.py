@@ -46,7 +46,8 @@ class ConfigInfo(ctypes.Structure):
                 ("trans_a", ctypes.c_int), ("trans_b", ctypes.c_int),
                 ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
                 ("stages", ctypes.c_int), ("lds_bytes", ctypes.c_int), ("occupancy", ctypes.c_int),
-                ("persistent", ctypes.c_int)]
+                ("persistent", ctypes.c_int), ("streamk", ctypes.c_int),
+                ("bres", ctypes.c_int)]
 
 
 class TuneResult(ctypes.Structure):
@@ -308,8 +309,9 @@ def conv2d_fwd(x, w, stride=(1, 1), padding="SAME", out=None, workspace=None):
     """NHWC x (N, H, W, Cin) convolved with HWIO w (KH, KW, Cin, Cout).
 
     ``padding`` is 'SAME', 'VALID' or (top, left, bottom, right).  The
-    workspace (a float32 device tensor) is optional; it lets small outputs
-    split their reduction (see ``conv2d_workspace_bytes``).
+    workspace (a float32 device tensor) lets the reduction be split across
+    work-groups (split-K or stream-K, see ``conv2d_workspace_bytes``); when
+    None, one of the size the chosen configuration needs is allocated.
     """
     import torch
     _check_f32_cuda(x, "x")
@@ -331,6 +333,10 @@ def conv2d_fwd(x, w, stride=(1, 1), padding="SAME", out=None, workspace=None):
     if tuple(out.shape) != (N, Ho, Wo, Cout) or not out.is_contiguous():
         raise ValueError("out must be a contiguous %s tensor" % ((N, Ho, Wo, Cout),))
     ws_ptr, ws_bytes = None, 0
+    if workspace is None:
+        need = conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, sh, sw, pt, pl, pb, pr)
+        if need:
+            workspace = torch.empty((need + 3) // 4, dtype=torch.float32, device=x.device)
     if workspace is not None:
         _check_f32_cuda(workspace, "workspace")
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * 4
@@ -413,6 +419,10 @@ def tune_conv2d(x, w, stride=(1, 1), padding="SAME", out=None, workspace=None, i
     if out is None:
         out = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device=x.device)
     ws_ptr, ws_bytes = None, 0
+    if workspace is None:
+        need = conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, sh, sw, pt, pl, pb, pr)
+        if need:
+            workspace = torch.empty((need + 3) // 4, dtype=torch.float32, device=x.device)
     if workspace is not None:
         _check_f32_cuda(workspace, "workspace")
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * 4

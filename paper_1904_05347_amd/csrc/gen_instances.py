@@ -35,11 +35,32 @@ CONV_PERSISTENT = [
     (64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 32, 2, 2, 4, 4, 1), (128, 64, 16, 2, 2, 4, 4, 1),
     (128, 128, 16, 2, 4, 4, 4, 2), (128, 128, 32, 2, 4, 4, 4, 2), (256, 128, 16, 4, 2, 4, 4, 2),
 ]
+# Stream-K forms (resident work-groups share the (tile, K-block) iterations
+# evenly; partial tiles are finished by their last contributor).  They need a
+# workspace, so they serve convolutions (the 1x1 stride-1 layers run the NN
+# GEMM instances through the convolution call).
+GEMM_STREAMK = [
+    (64, 64, 32, 2, 2, 4, 4, 1), (128, 64, 32, 2, 2, 4, 4, 1), (128, 128, 32, 2, 4, 4, 4, 2),
+    (256, 128, 32, 4, 2, 4, 4, 2),
+]
+CONV_STREAMK = [
+    (64, 64, 32, 2, 2, 4, 4, 1), (128, 64, 32, 2, 2, 4, 4, 1), (128, 128, 32, 2, 4, 4, 4, 2),
+    (256, 128, 32, 4, 2, 4, 4, 2), (256, 256, 16, 2, 4, 4, 4, 2),
+]
+# B-resident streaming forms (NN only; K == BK and N == BN exactly): the
+# 1x1 convolutions with 64 input channels and 64 or 256 output channels.
+GEMM_BRES = [(64, 64, 64, 2, 2, 1), (128, 64, 64, 4, 1, 1), (64, 256, 64, 2, 4, 2), (32, 256, 64, 1, 8, 2)]
 # Ablation forms (NN only): 2-wide and 4-byte loads of a 128 x 128 tile beside
 # its 16-byte form, and single-LDS-stage (not double-buffered) twins of
 # instances the benchmarks use ("_s1").
 ABLATION_TILES = [(128, 128, 16, 2, 2, 2, 2, 1), (128, 128, 16, 2, 2, 1, 1, 1)]
 SINGLE_STAGE = [(128, 128, 16, 2, 2, 4, 4, 1), (64, 64, 32, 2, 2, 4, 4, 1), (256, 256, 32, 2, 4, 4, 4, 2)]
+# NN-only tiles for short reductions (1x1 layers with K = 64 .. 256): the
+# whole reduction in one or few K-blocks, single LDS stage so that more
+# work-groups fit on a CU, and full-width tiles for N = 256.
+NN_SHORT_K = [(64, 64, 64, 2, 2, 4, 4, 1), (128, 64, 64, 2, 2, 4, 4, 1), (64, 256, 32, 1, 4, 4, 4, 1),
+              (128, 256, 32, 2, 4, 4, 4, 2)]
+NN_SHORT_K_1S = [(64, 64, 64, 2, 2, 4, 4, 1), (128, 64, 64, 2, 2, 4, 4, 1), (128, 128, 64, 2, 4, 4, 4, 2)]
 
 # TT only needs a large, a small and a scalar-load tile.
 TT_TILES = [(128, 128, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 1, 1, 1)]
@@ -59,10 +80,11 @@ CONV_TILES = [
     (128, 128, 64, 2, 4, 4, 4, 2),
     (128, 64, 16, 2, 2, 1, 4, 1), (256, 64, 16, 4, 1, 1, 4, 1),
     (64, 64, 16, 2, 2, 1, 1, 1),
+    (64, 64, 64, 2, 2, 4, 4, 1), (128, 64, 64, 2, 2, 4, 4, 1),
 ]
 
 
-def _name(kind, t, layout=None, persistent=False, single=False):
+def _name(kind, t, layout=None, persistent=False, single=False, streamk=False):
     bm, bn, bk, wm, wn, va, vb, occ = t
     s = "%s_%dx%dx%d_w%dx%d" % (kind, bm, bn, bk, wm, wn)
     if layout:
@@ -74,6 +96,8 @@ def _name(kind, t, layout=None, persistent=False, single=False):
         s += "_p"
     if single:
         s += "_s1"
+    if streamk:
+        s += "_sk"
     return s
 
 
@@ -112,11 +136,24 @@ def main():
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM_P(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
                            % (_name("gemm", t, layout, True), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
+        for t in (GEMM_STREAMK if layout == "nn" else []):
+            bm, bn, bk, wm, wn, va, vb, occ = t
+            entries.append("PK_GEMM_SK(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
+                           % (_name("gemm", t, layout, streamk=True), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
+        for t in (GEMM_BRES if layout == "nn" else []):
+            bm, bn, bk, wm, wn, occ = t
+            entries.append("PK_GEMM_BRES(%s, %d, %d, %d, %d, %d, %d)"
+                           % ("gemm_%dx%dx%d_w%dx%d_nn_v44%s_br" % (bm, bn, bk, wm, wn, "_o%d" % occ if occ > 1 else ""),
+                              bm, bn, bk, wm, wn, occ))
         for t in (ABLATION_TILES if layout == "nn" else []):
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
                            % (_name("gemm", t, layout), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
-        for t in (SINGLE_STAGE if layout == "nn" else []):
+        for t in (NN_SHORT_K if layout == "nn" else []):
+            bm, bn, bk, wm, wn, va, vb, occ = t
+            entries.append("PK_GEMM(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
+                           % (_name("gemm", t, layout), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
+        for t in (SINGLE_STAGE + NN_SHORT_K_1S if layout == "nn" else []):
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM_1S(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
                            % (_name("gemm", t, layout, single=True), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
@@ -131,6 +168,10 @@ def main():
         bm, bn, bk, wm, wn, va, vb, occ = t
         entries.append("PK_CONV_P(%s, %d, %d, %d, %d, %d, %d, %d, %d)"
                        % (_name("conv", t, None, True), bm, bn, bk, wm, wn, va, vb, occ))
+    for t in CONV_STREAMK:
+        bm, bn, bk, wm, wn, va, vb, occ = t
+        entries.append("PK_CONV_SK(%s, %d, %d, %d, %d, %d, %d, %d, %d)"
+                       % (_name("conv", t, streamk=True), bm, bn, bk, wm, wn, va, vb, occ))
     _file("pk_inst_conv.hip", "implicit-GEMM convolution instances (A gathered from an NHWC "
           "image, B the HWIO filter viewed as (KH*KW*Cin) x Cout).", "configs_conv", entries)
 

@@ -157,9 +157,9 @@ const TunedShape kTuned[] = {
     {0, 0, 0, 1024, 1024, 1024, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
     // VGG-16 block-first layers at batch 32 (3x3, stride 1)
     {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
-    {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
-    {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44", 1},
-    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 6},
+    {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
+    {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
+    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
     // ResNet-50 bottleneck layers at batch 32
     {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},
     {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x64_w2x4_v44_o2", 1},
@@ -242,6 +242,9 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, bool 
     return find_config(name);
 }
 
+// A B-resident configuration runs only the product its LDS holds whole.
+bool bres_fits(const Config *c, int64_t N, int64_t K) { return !c->bres || (N == c->bn && K == c->bk); }
+
 bool conv_config_fits(const Config *c, bool va4, bool vb4)
 {
     if (c->kind == pk::KIND_DIRECT) return true;  // checked against the window by the caller
@@ -274,6 +277,7 @@ const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4)
 // 14x14x512 layer at batch 32.
 int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 {
+    if (c->bres) return 1;  // its one K-block is the whole reduction
     const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
     const int64_t nkb = ceil_div(K, c->bk);
     if (tiles >= 4 * kCUs) return 1;
@@ -282,6 +286,42 @@ int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
     if (s > max_by_k) s = max_by_k;
     if (s > 16) s = 16;
     return s < 1 ? 1 : (int)s;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+int xcd_count()
+{
+    const int x = env_int("PK_XCDS", 8);
+    return x < 1 ? 1 : x;
+}
+
+// Stream-K plan of an M x N x K product on configuration c: tiles, K-blocks
+// per tile, work-groups (the CUs' resident capacity, at most one per
+// iteration, a multiple of the XCD count) and the workspace layout: 2 partial
+// tiles per work-group, then one arrival counter per tile (256-byte aligned).
+struct SkPlan {
+    int tiles, nkb, groups;
+    size_t cnt_off, bytes;
+};
+
+bool streamk_plan(const Config *c, int64_t M, int64_t N, int64_t K, SkPlan *pl)
+{
+    if (!c->streamk || !c->resident) return false;
+    const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
+    const int64_t nkb = ceil_div(K, c->bk);
+    if (tiles < 1 || nkb < 1 || tiles * nkb >= ((int64_t)1 << 31)) return false;
+    int64_t g = (int64_t)c->resident(0) * pk::device_cu_count();
+    if (g > tiles * nkb) g = tiles * nkb;
+    const int x = xcd_count();
+    if (x > 1 && g >= x) g -= g % x;
+    if (g < 1) return false;
+    pl->tiles = (int)tiles;
+    pl->nkb = (int)nkb;
+    pl->groups = (int)g;
+    pl->cnt_off = align256((size_t)2 * g * c->bm * c->bn * sizeof(float));
+    pl->bytes = pl->cnt_off + (size_t)tiles * sizeof(int);
+    return true;
 }
 
 void fill_common(KernelArgs &a, const Config *c, int64_t M, int64_t N, int64_t K, int splits)
@@ -297,8 +337,7 @@ void fill_common(KernelArgs &a, const Config *c, int64_t M, int64_t N, int64_t K
     a.kblocks_per_split = (int)ceil_div(nkb, splits);
     a.splits = (int)ceil_div(nkb, a.kblocks_per_split);
     if (a.splits < 1) a.splits = 1;
-    a.xcds = env_int("PK_XCDS", 8);
-    if (a.xcds < 1) a.xcds = 1;
+    a.xcds = xcd_count();
     a.group_m = env_int("PK_GROUP_M", 8);
     if (a.group_m < 1) a.group_m = 1;
 }
@@ -392,6 +431,8 @@ int pk_get_config(int idx, pk_config_info *info)
     info->lds_bytes = c->lds_bytes;
     info->occupancy = c->occupancy;
     info->persistent = c->persistent;
+    info->streamk = c->streamk;
+    info->bres = c->bres;
     return PK_OK;
 }
 
@@ -488,12 +529,13 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float al
     const Config *c = forced(&bad);
     if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
     if (c) {
-        if (!gemm_config_fits(c, ta, tb, vec_ok)) return PK_ERR_NOT_SUPPORTED;
+        // stream-K needs a workspace, which this call does not take
+        if (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K)) return PK_ERR_NOT_SUPPORTED;
     } else {
         TunedShape tbuf;
         const TunedShape *t = find_tuned(0, ta, tb, M, N, K, 0, 0, &tbuf) ? &tbuf : nullptr;
         c = t ? find_config(t->config) : nullptr;
-        if (c && !gemm_config_fits(c, ta, tb, vec_ok)) c = nullptr;
+        if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K))) c = nullptr;
         if (!c) c = select_gemm(ta, tb, M, N, K, vec_ok);
         if (!c) return PK_ERR_NOT_SUPPORTED;
     }
@@ -525,17 +567,27 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
     const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
     const int64_t M = checked_mul3(N, Ho, Wo), K = checked_mul3(KH, KW, Cin);
     if (M < 0 || K < 0 || M > kMaxDim || K > kMaxDim || Cout > kMaxDim) return 0;
-    // the selector's choice for 16-byte aligned tensors (what the allocator gives)
+    // the choice the next call on this thread makes for 16-byte aligned
+    // tensors (what the allocator gives): a forced configuration, else the
+    // measured one, else the rules
     const bool v4 = Cin % 4 == 0 && Cout % 4 == 0;
+    bool bad = false;
+    const Config *c = forced(&bad);
+    if (bad) return 0;
+    const TunedShape *tuned = nullptr;
     TunedShape tbuf;
-    const TunedShape *tuned =
-        (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
-    const bool direct_ok = !gemm_path && pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535;
-    if (direct_ok && !(tuned && v4)) return 0;
-    const Config *c = (tuned && v4) ? find_config(tuned->config) : nullptr;
-    if (c && c->kind == pk::KIND_DIRECT) return 0;
-    if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
-    if (!c) return 0;
+    if (!c) {
+        tuned = (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
+        const bool direct_ok = !gemm_path && pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535;
+        if (direct_ok && !(tuned && v4)) return 0;
+        c = (tuned && v4) ? find_config(tuned->config) : nullptr;
+        if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
+    }
+    if (!c || c->kind == pk::KIND_DIRECT) return 0;
+    if (c->streamk) {
+        SkPlan plan;
+        return streamk_plan(c, M, Cout, K, &plan) ? plan.bytes : 0;
+    }
     if (tuned && v4 && tuned->splits > 0 && t_forced_splits == 0)
         return tuned->splits > 1 ? (size_t)tuned->splits * (size_t)M * (size_t)Cout * sizeof(float) : 0;
     const int splits = t_forced_splits > 0 ? t_forced_splits : choose_splits(c, M, Cout, K);
@@ -603,24 +655,26 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     bool bad = false;
     const Config *c = forced(&bad);
     if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
+    const bool was_forced = c != nullptr;
 
     const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
     TunedShape tbuf;
     const TunedShape *tuned =
         (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
+    // 1x1, stride 1, no padding: the image is already the M x Cin matrix
+    const bool vec_ok = gemm_path && gemm_vec_ok(0, 0, M, Cout, Cin, x, Cin, f, Cout);
+    const bool va4 = Cin % 4 == 0 && aligned16(x);
+    const bool vb4 = Cout % 4 == 0 && aligned16(f);
     if (gemm_path) {
-        // 1x1, stride 1, no padding: the image is already the M x Cin matrix.
-        const bool vec_ok = gemm_vec_ok(0, 0, M, Cout, Cin, x, Cin, f, Cout);
         if (c) {
-            if (!gemm_config_fits(c, 0, 0, vec_ok)) return PK_ERR_NOT_SUPPORTED;
+            if (!gemm_config_fits(c, 0, 0, vec_ok) || !bres_fits(c, Cout, Cin)) return PK_ERR_NOT_SUPPORTED;
         } else {
             c = (tuned && vec_ok) ? find_config(tuned->config) : nullptr;
+            if (c && !bres_fits(c, Cout, Cin)) c = nullptr;
             if (!c) c = select_gemm(0, 0, M, Cout, Cin, vec_ok);
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     } else {
-        const bool va4 = Cin % 4 == 0 && aligned16(x);
-        const bool vb4 = Cout % 4 == 0 && aligned16(f);
         const bool direct_ok = pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535;
         if (c) {
             if (!conv_config_fits(c, va4, vb4)) return PK_ERR_NOT_SUPPORTED;
@@ -646,6 +700,33 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         a.KH = (int)KH;
         a.batch = (int)N;
     }
+    // stream-K needs its partial tiles and counters in the workspace; without
+    // room for them the rules choose again (a forced choice reports it)
+    SkPlan skp;
+    bool streamk = false;
+    if (c->streamk) {
+        const bool planned = streamk_plan(c, M, Cout, K, &skp);
+        if (planned && workspace && workspace_bytes >= skp.bytes && aligned16(workspace)) {
+            streamk = true;
+        } else if (was_forced) {
+            return planned ? PK_ERR_WORKSPACE : PK_ERR_NOT_SUPPORTED;
+        } else {
+            c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, vec_ok) : select_conv(M, Cout, va4, vb4);
+            if (!c) return PK_ERR_NOT_SUPPORTED;
+        }
+    }
+    if (streamk) {
+        a.A = x;
+        a.lda = Cin;
+        fill_common(a, c, M, Cout, K, 1);
+        const uintptr_t w0 = (uintptr_t)workspace, w1 = w0 + skp.bytes;
+        if (overlap(w0, w1, x0, x1) || overlap(w0, w1, f0, f1) || overlap(w0, w1, y0, y1)) return invalid(19);
+        a.sk_nkb = skp.nkb;
+        a.sk_groups = skp.groups;
+        a.sk_part = (float *)workspace;
+        a.sk_cnt = (int *)((char *)workspace + skp.cnt_off);
+        return launch(c, a, s);
+    }
     if (c->kind == pk::KIND_DIRECT) {
         a.A = x;
         a.M = (int)M;
@@ -660,6 +741,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     const size_t per_split = (size_t)M * (size_t)Cout * sizeof(float);
     if (t_forced_splits > 0) {
         splits = t_forced_splits;
+        if (splits > 1 && c->bres) return PK_ERR_NOT_SUPPORTED;
         if (splits > 1 && (!workspace || workspace_bytes < (size_t)splits * per_split)) return PK_ERR_WORKSPACE;
     } else {
         const bool tuned_cfg = tuned && strcmp(c->name, tuned->config) == 0 && tuned->splits > 0;
@@ -688,8 +770,6 @@ struct WinoPlan {
     int64_t Ho, Wo, TH, TW, T;
     size_t off_u, off_v, off_m, bytes;
 };
-
-size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 // false when the sizes overflow the kernels' indexing.
 bool wino_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Cin, int64_t Cout, WinoPlan *w)
@@ -723,7 +803,7 @@ const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok
     (void)Cout;
     const Config *c = forced(bad);
     if (*bad) return nullptr;
-    if (c) return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent) ? c : nullptr;
+    if (c) return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent && !c->streamk && !c->bres) ? c : nullptr;
     if (!vec_ok) return find_config("gemm_64x64x16_w2x2_nn_v11");
     return find_config(Cin <= 128 ? "gemm_64x64x16_w2x2_nn_v44" : "gemm_64x64x32_w2x2_nn_v44");
 }
@@ -950,7 +1030,8 @@ int pk_tune_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, flo
         const Config *cfgs = pk::configs(&n);
         for (int i = 0; i < n; ++i) {
             const Config *c = &cfgs[i];
-            if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb || c->single_stage) continue;
+            if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb || c->single_stage || c->streamk)
+                continue;
             scope.force(c, 0);
             const float ms = time_calls(
                 [&] { return pk_sgemm(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream); },
@@ -1009,7 +1090,8 @@ int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t 
                                          : (c->kind == pk::KIND_CONV || c->kind == pk::KIND_DIRECT);
             if (!takes) continue;
             for (int sp : kSplits) {
-                if (sp > 1 && (c->kind == pk::KIND_DIRECT || workspace_bytes < (size_t)sp * M * Cout * sizeof(float)))
+                if (sp > 1 && (c->kind == pk::KIND_DIRECT || c->streamk ||
+                               workspace_bytes < (size_t)sp * M * Cout * sizeof(float)))
                     break;
                 scope.force(c, sp);
                 const float ms = time_calls(call, iters, s, ev, &st);

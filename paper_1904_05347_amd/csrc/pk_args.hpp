@@ -25,6 +25,12 @@ struct KernelArgs {
     // C + b*stride_c (elements).  0 = one product.
     int nbatch;
     int64_t stride_a, stride_b, stride_c;
+    // stream-K launches: K-blocks per tile, partial-tile slots (2 per
+    // work-group, BM x BN floats each) and one arrival counter per tile, both
+    // in the caller's workspace; the counters are zeroed before each launch.
+    int sk_nkb, sk_groups;  // sk_groups: the launch's work-groups (host side)
+    float *sk_part;
+    int *sk_cnt;
 };
 
 }  // namespace pk

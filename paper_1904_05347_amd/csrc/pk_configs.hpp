@@ -30,6 +30,11 @@ struct Config {
     int lds_bytes;
     LaunchFn launch;
     int single_stage;  // 1 = one LDS stage (no double buffering; an ablation form)
+    int streamk;       // 1 = stream-K: resident work-groups share the (tile, K-block) iterations evenly
+    // work-groups of this instance one CU holds at once (occupancy query;
+    // beta != 0 selects the epilogue that reads C).  Set for stream-K instances.
+    int (*resident)(int beta);
+    int bres;  // 1 = op(B) resident in LDS: runs only products with K == bk and N == bn
 };
 
 // The registry (defined with the kernel instances, host side only).
@@ -45,6 +50,8 @@ int device_cu_count();
 bool direct_conv_fits(int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t sw);
 
 hipError_t launch_scale(float *C, int M, int N, int64_t ldc, float beta, hipStream_t stream);
+// p[0 .. n) = 0 (a kernel, so that it may be captured in a graph).
+hipError_t launch_zero_ints(int *p, int n, hipStream_t stream);
 
 // Winograd F(2x2, 3x3) transforms (pk_winograd.hip).  U: 16 x Cin x Cout,
 // V: 16 x T x Cin, M: 16 x T x Cout, T = N * TH * TW tiles of 2 x 2 outputs.

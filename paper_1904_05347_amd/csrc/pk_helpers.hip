@@ -34,6 +34,13 @@ __global__ void __launch_bounds__(256) scale_kernel(float *C, int M, int N, int6
     }
 }
 
+// Arrival counters of a stream-K launch start at zero.
+__global__ void __launch_bounds__(256) zero_ints_kernel(int *p, int n)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
+}
+
 // ---------------------------------------------------------------- helpers
 
 int device_cu_count()
@@ -65,6 +72,13 @@ hipError_t launch_scale(float *C, int M, int N, int64_t ldc, float beta, hipStre
     const int64_t blocks = (total + 255) / 256;
     const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);
     hipLaunchKernelGGL(scale_kernel, dim3(grid), dim3(256), 0, stream, C, M, N, ldc, beta);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_ints(int *p, int n, hipStream_t stream)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_ints_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, p, n);
     return hipGetLastError();
 }
 

@@ -58,6 +58,70 @@ static hipError_t launch_gemm_persistent(const KernelArgs &a, hipStream_t stream
     return hipGetLastError();
 }
 
+// Stream-K: work-groups one CU holds at once, per epilogue form.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+static int resident_streamk(int beta)
+{
+    static int per_cu[2] = {0, 0};  // the same on every MI355X
+    const int b = beta ? 1 : 0;
+    if (per_cu[b] == 0) {
+        auto kernel = gemm_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, false>;
+        if constexpr (AMODE != A_CONV) {
+            if (b) kernel = gemm_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, true>;
+        }
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, 64 * WAVES_M * WAVES_N, 0) != hipSuccess ||
+            n < 1)
+            n = 1;
+        per_cu[b] = n;
+    }
+    return per_cu[b];
+}
+
+// Stream-K launch: a.sk_groups work-groups (planned by the caller together
+// with the workspace), after zeroing the tiles' arrival counters.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+static hipError_t launch_gemm_streamk(const KernelArgs &a, hipStream_t stream)
+{
+    if (a.sk_groups < 1 || !a.sk_part || !a.sk_cnt || a.sk_nkb < 1) return hipErrorInvalidValue;
+    const hipError_t z = launch_zero_ints(a.sk_cnt, a.tiles_m * a.tiles_n, stream);
+    if (z != hipSuccess) return z;
+    const dim3 grid((unsigned)a.sk_groups), block(64 * WAVES_M * WAVES_N);
+    if constexpr (AMODE != A_CONV) {
+        if (reads_c<AMODE>(a)) {
+            hipLaunchKernelGGL((gemm_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, true>),
+                               grid, block, 0, stream, a);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((gemm_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, false>),
+                       grid, block, 0, stream, a);
+    return hipGetLastError();
+}
+
+// B-resident streaming launch: as many work-groups as the CUs hold (at most
+// one per BM-row tile), each walking a contiguous range of tiles.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int OCC>
+static hipError_t launch_gemm_bres(const KernelArgs &a, hipStream_t stream)
+{
+    if (a.K != BK || a.N != BN || a.splits > 1 || a.nbatch > 1) return hipErrorInvalidValue;
+    const bool beta = reads_c<A_KCONTIG>(a);
+    auto kernel = beta ? gemm_bres_kernel<BM, BN, BK, WAVES_M, WAVES_N, OCC, true>
+                       : gemm_bres_kernel<BM, BN, BK, WAVES_M, WAVES_N, OCC, false>;
+    const int threads = 64 * WAVES_M * WAVES_N;
+    static int per_cu[2] = {0, 0};
+    if (per_cu[beta] == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
+        per_cu[beta] = n;
+    }
+    const int64_t tiles = (a.M + BM - 1) / BM;
+    int64_t grid = (int64_t)per_cu[beta] * device_cu_count();
+    if (grid > tiles) grid = tiles;
+    hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(threads), 0, stream, a);
+    return hipGetLastError();
+}
+
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
 static hipError_t launch_gemm_single_stage(const KernelArgs &a, hipStream_t stream)
 {
@@ -107,5 +171,29 @@ static constexpr int lds_bytes()
      lds_bytes<BM, BN, BK, WM, WN, A_CONV, false, VA, VB>(),                                          \
      &launch_gemm_persistent<BM, BN, BK, WM, WN, A_CONV, false, VA, VB, OCC>}
 
+
+// LDS of the B-resident form: two A stages and B transposed.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N>
+static constexpr int bres_lds_bytes()
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, true, 4, 4> G;
+    return (int)sizeof(float) * (2 * G::A_STAGE + G::B_STAGE);
+}
+
+#define PK_GEMM_BRES(name, BM, BN, BK, WM, WN, OCC)                                                    \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, 0, 0, 4, 4, OCC, 0, bres_lds_bytes<BM, BN, BK, WM, WN>(),   \
+     &launch_gemm_bres<BM, BN, BK, WM, WN, OCC>, 0, 0, nullptr, 1}
+
+#define PK_GEMM_SK(name, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC)                                      \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC, 0,                                    \
+     lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),                \
+     &launch_gemm_streamk<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>, 0, 1, \
+     &resident_streamk<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>}
+
+#define PK_CONV_SK(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                              \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 0,                                      \
+     lds_bytes<BM, BN, BK, WM, WN, A_CONV, false, VA, VB>(),                                          \
+     &launch_gemm_streamk<BM, BN, BK, WM, WN, A_CONV, false, VA, VB, OCC>, 0, 1,                      \
+     &resident_streamk<BM, BN, BK, WM, WN, A_CONV, false, VA, VB, OCC>}
 
 }  // namespace pk

@@ -780,4 +780,306 @@ gemm_persistent_kernel(KernelArgs p)
     }
 }
 
+
+// Stream-K partition of a product's T = tiles * nkb (tile, K-block)
+// iterations over G work-groups: logical work-group g owns the contiguous
+// iterations [start(g), start(g+1)) with start(g) = floor(g*T/G), so every
+// work-group does the same amount of MFMA work to within one K-block,
+// whatever the tile count.  Tile t (iterations [t*nkb, (t+1)*nkb)) is
+// computed by the work-groups owner(t*nkb) .. owner((t+1)*nkb - 1), each
+// summing a contiguous run of its K-blocks (the blocked identity over a
+// partition of K, Section 3.1.1).  A work-group's first and last tile may be
+// such partial tiles; their partial sums go to slot 2g and 2g+1.
+struct StreamK {
+    int T, G, nkb;
+
+    __device__ __forceinline__ int start(int g) const { return (int)(((int64_t)g * T) / G); }
+    // the work-group whose range holds iteration i: the largest g with start(g) <= i
+    __device__ __forceinline__ int owner(int i) const { return (int)(((int64_t)(i + 1) * G + T - 1) / T) - 1; }
+    __device__ __forceinline__ int slot(int g, int t) const { return start(g) / nkb == t ? 2 * g : 2 * g + 1; }
+};
+
+// Stream-K form of the persistent contraction.  The grid is the resident
+// work-groups; each runs the one-barrier K pipeline over its iteration range,
+// across tile boundaries.  A tile whose K-blocks all fall in one range is
+// finished as usual.  A partial tile's sum is written to the range's slot;
+// the work-group that arrives last at the tile's counter (agent-scope atomic)
+// adds the partial sums of all its contributors in the order of their K-blocks
+// and writes C, so the result does not depend on which one finishes last and
+// no work-group ever waits for another.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC, bool BETA>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_streamk_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
+    typedef typename G::ALoader ALoader;
+    typedef typename G::BLoader BLoader;
+    constexpr int NT = G::NT;
+
+    __shared__ __attribute__((aligned(16))) float smem[G::LDS_FLOATS];
+    __shared__ int s_arrival;
+    float *As = smem;
+    float *Bs = smem + 2 * G::A_STAGE;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+    const int nkb = p.sk_nkb;
+    const StreamK sk{p.tiles_m * p.tiles_n * nkb, (int)gridDim.x, nkb};
+
+    // work-group b runs on XCD b % xcds: give each XCD a contiguous share of
+    // the logical ranges, so the tiles an XCD works on are neighbours
+    int lg = blockIdx.x;
+    if (p.xcds > 1 && sk.G % p.xcds == 0) lg = (blockIdx.x % p.xcds) * (sk.G / p.xcds) + blockIdx.x / p.xcds;
+    const int end = sk.start(lg + 1);
+    int seg = sk.start(lg);  // first iteration of the current segment
+    if (seg >= end) return;  // uniform over the work-group, before any barrier
+
+    int tile = seg / nkb;
+    int kbeg = seg - tile * nkb;
+    int kend = min(nkb, kbeg + (end - seg));
+    int m0, n0;
+    auto decode_tile = [&](int t, int &m0_, int &n0_) {
+        int tm, tn;
+        tile_of(p, t, tm, tn);
+        m0_ = tm * BM;
+        n0_ = tn * BN;
+    };
+    decode_tile(tile, m0, n0);
+    int kb = kbeg;
+
+    ALoader la;
+    BLoader lb;
+    auto init_loaders = [&](int m0_, int n0_, int kbeg_) {
+        if constexpr (AMODE == A_CONV)
+            la.init(p, m0_, kbeg_, tid);
+        else
+            la.init(p.A, p.lda, m0_, p.M, kbeg_, tid);
+        lb.init(p.B, p.ldb, n0_, p.N, kbeg_, tid);
+    };
+    init_loaders(m0, n0, kb);
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename ALoader::VT ra[ALoader::LOADS];
+    typename BLoader::VT rb[BLoader::LOADS];
+
+    la.load(ra, kb * BK, p.K);
+    lb.load(rb, kb * BK, p.K);
+    la.advance();
+    lb.advance();
+    la.template store<G::LDA_S>(As, ra, tid);
+    lb.template store<G::LDB_S>(Bs, rb, tid);
+    __syncthreads();
+
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NGR = G::NG;
+    int stage = 0;
+    G::read_group(As, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
+
+    for (;;) {
+        const bool last_block = kb + 1 >= kend;
+        int ntile = tile, nm0 = m0, nn0 = n0, nkbeg = kbeg, nkend = kend, nkb1 = kb + 1, nseg = seg;
+        bool more = true;
+        if (last_block) {
+            nseg = seg + (kend - kbeg);
+            more = nseg < end;
+            if (more) {
+                ntile = nseg / nkb;
+                nkbeg = nseg - ntile * nkb;
+                nkend = min(nkb, nkbeg + (end - nseg));
+                decode_tile(ntile, nm0, nn0);
+                nkb1 = nkbeg;
+            }
+        }
+        if (more) {
+            if (last_block) init_loaders(nm0, nn0, nkb1);
+            la.load(ra, nkb1 * BK, p.K);
+            lb.load(rb, nkb1 * BK, p.K);
+            la.advance();
+            lb.advance();
+        }
+        const float *as = As + stage * G::A_STAGE;
+        const float *bs = Bs + stage * G::B_STAGE;
+#pragma unroll
+        for (int g = 0; g < NGR - 1; ++g) {
+            G::read_group(as, bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        if (more) {
+            la.template store<G::LDA_S>(As + (stage ^ 1) * G::A_STAGE, ra, tid);
+            lb.template store<G::LDB_S>(Bs + (stage ^ 1) * G::B_STAGE, rb, tid);
+        }
+        __syncthreads();
+        G::read_group(As + (stage ^ 1) * G::A_STAGE, Bs + (stage ^ 1) * G::B_STAGE, a_row, b_row, h, 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NGR - 1) & 1], fb[(NGR - 1) & 1]);
+        if (last_block) {
+            const int row_base = m0 + wm * G::WM + 4 * h, col_base = n0 + wn * G::WN + l32;
+            bool write = true;  // this work-group writes the tile's C block
+            if (kbeg != 0 || kend != nkb) {
+                // partial tile: publish this range's sum.  Value r of block
+                // (i, j) of thread t sits at float ((i*RN + j)*16 + r)*NT + t
+                // of the slot (each store instruction of a wave writes 256
+                // contiguous bytes).  The partial sums are written and read
+                // with agent-scope atomic accesses, which the hardware keeps
+                // coherent across the XCDs' L2 caches, so no cache-wide
+                // write-back or invalidation is needed; each wave waits for
+                // its stores to complete before the work-group counts itself
+                // in.
+                float *mine = p.sk_part + (int64_t)sk.slot(lg, tile) * (BM * BN) + tid;
+                // the per-element offsets below are constants; without this the
+                // compiler hoists all RM*RN*16 addresses out of the tile loop
+                // and keeps them in registers
+                asm volatile("" : "+v"(mine));
+#pragma unroll
+                for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                    for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r)
+                            __hip_atomic_store(mine + ((i * G::RN + j) * 16 + r) * NT, acc[i][j][r],
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
+                __syncthreads();
+                if (tid == 0)
+                    s_arrival = __hip_atomic_fetch_add(p.sk_cnt + tile, 1, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                __syncthreads();
+                const int lo = sk.owner(tile * nkb), hi = sk.owner(tile * nkb + nkb - 1);
+                write = s_arrival == hi - lo;  // the last contributor: uniform over the work-group
+                if (write) {
+                    // sum the contributors' partial sums in K-block order (its own
+                    // re-read like the others), so the bits do not depend on
+                    // which contributor adds them
+                    // (the first contributor's load redefines acc whole, so the
+                    // values the MFMAs left there are dead from here on)
+                    auto gather = [&](int g, bool first) {
+                        const float *src = p.sk_part + (int64_t)sk.slot(g, tile) * (BM * BN) + tid;
+                        asm volatile("" : "+v"(src));
+#pragma unroll
+                        for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                            for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                                for (int r = 0; r < 16; ++r) {
+                                    const float v = __hip_atomic_load(src + ((i * G::RN + j) * 16 + r) * NT,
+                                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                    acc[i][j][r] = first ? v : acc[i][j][r] + v;
+                                }
+                    };
+                    gather(lo, true);
+                    for (int g = lo + 1; g <= hi; ++g) gather(g, false);
+                }
+            }
+            if (write) G::template store<BETA>(p, acc, row_base, col_base, 0);
+            G::zero(acc);
+        }
+        if (!more) break;
+        tile = ntile;
+        m0 = nm0;
+        n0 = nn0;
+        kbeg = nkbeg;
+        kend = nkend;
+        kb = nkb1;
+        seg = nseg;
+        stage ^= 1;
+    }
+}
+
+
+// Contraction with op(B) resident in LDS, for short reductions (the 1x1
+// convolutions of ResNet-50's bottlenecks: K = 64 input channels, N = 64 or
+// 256 output channels).  There the whole of B is one K-block and at most
+// 64 KB, while A and C stream through HBM once (8-16 flop per byte), so the
+// time goes to memory, not to the MFMAs.  A persistent work-group loads B
+// once (stored n-major, k contiguous, for 16-byte operand reads), then walks
+// a contiguous range of BM-row tiles of A: the next tile's rows are loaded
+// into registers while the current one is multiplied, and the current tile's
+// C stores drain while the next one computes.  K == BK and N == BN exactly
+// (the launcher checks); M is arbitrary.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int OCC, bool BETA>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_bres_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, true, 4, 4> G;
+    typedef typename G::ALoader ALoader;
+    constexpr int NT = G::NT;
+    static_assert(BN % 4 == 0 && (BK * BN / 4) % NT == 0, "B staging");
+
+    __shared__ __attribute__((aligned(16))) float smem[2 * G::A_STAGE + G::B_STAGE];
+    float *As = smem;                   // [2][BM][BK + PAD]
+    float *Bs = smem + 2 * G::A_STAGE;  // [BN][BK + PAD]: B transposed
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+
+    const int tiles = (p.M + BM - 1) / BM;
+    const int t0 = (int)(((int64_t)blockIdx.x * tiles) / gridDim.x);
+    const int t1 = (int)(((int64_t)(blockIdx.x + 1) * tiles) / gridDim.x);
+    if (t0 >= t1) return;  // uniform over the work-group, before any barrier
+
+    // B: BK x BN row-major in global memory -> Bs[n][k]
+#pragma unroll
+    for (int i = 0; i < BK * BN / 4 / NT; ++i) {
+        const int c = tid + i * NT;
+        const int k = c / (BN / 4), n = (c % (BN / 4)) * 4;
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(p.B + (int64_t)k * p.ldb + n);
+        Bs[(n + 0) * G::LDB_S + k] = v[0];
+        Bs[(n + 1) * G::LDB_S + k] = v[1];
+        Bs[(n + 2) * G::LDB_S + k] = v[2];
+        Bs[(n + 3) * G::LDB_S + k] = v[3];
+    }
+    ALoader la;
+    typename ALoader::VT ra[ALoader::LOADS];
+    la.init(p.A, p.lda, t0 * BM, p.M, 0, tid);
+    la.load(ra, 0, p.K);
+    la.template store<G::LDA_S>(As, ra, tid);
+    __syncthreads();
+
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    typename G::Acc acc;
+    G::zero(acc);
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NGR = G::NG;
+    int stage = 0;
+    G::read_group(As, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
+
+    for (int t = t0; t < t1; ++t) {
+        const bool more = t + 1 < t1;
+        if (more) {
+            la.init(p.A, p.lda, (t + 1) * BM, p.M, 0, tid);
+            la.load(ra, 0, p.K);
+        }
+        const float *as = As + stage * G::A_STAGE;
+#pragma unroll
+        for (int g = 0; g < NGR - 1; ++g) {
+            G::read_group(as, Bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        if (more) la.template store<G::LDA_S>(As + (stage ^ 1) * G::A_STAGE, ra, tid);
+        __syncthreads();
+        // unconditional, as in gemm_kernel (after the last tile it reads a
+        // stage that is never used)
+        G::read_group(As + (stage ^ 1) * G::A_STAGE, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NGR - 1) & 1], fb[(NGR - 1) & 1]);
+        G::template store<BETA>(p, acc, t * BM + wm * G::WM + 4 * h, wn * G::WN + l32, 0);
+        G::zero(acc);
+        stage ^= 1;
+    }
+}
+
 }  // namespace pk

@@ -238,3 +238,62 @@ def test_paper_layer_suite(batch, case):
         ref, scale = oracle.conv2d_at(x, f, case.stride, case.pads, idx)
         assert_parity(out.reshape(-1)[idx], ref, scale, case.name + " " + cfg)
     assert np.all(np.isfinite(out))
+
+
+STREAMK_GEOMS = [
+    # (N, H, W, Cin, KH, KW, Cout, stride, pads)
+    (4, 24, 24, 64, 3, 3, 68, (1, 1), (1, 1, 1, 1)),   # many iterations per work-group, ragged Cout
+    (1, 9, 11, 8, 3, 3, 20, (1, 1), (1, 1, 1, 1)),     # fewer iterations than resident work-groups
+    (2, 14, 14, 64, 1, 1, 136, (1, 1), (0, 0, 0, 0)),  # 1x1 stride 1: the NN GEMM instances
+    (2, 15, 13, 32, 1, 1, 40, (2, 2), (0, 0, 0, 0)),   # strided 1x1: row gather
+]
+
+
+def test_streamk_configs_partial_tiles():
+    """Every stream-K configuration on problems whose (tile, K-block)
+    iterations cut tiles between work-groups: NaN-prefilled output, whole
+    output bit-exact against the oracle on integer data (a lost, doubled or
+    misplaced partial sum shows), and a second call gives the same bits."""
+    torch, pk = require_gpu()
+    ran = 0
+    for gi, (N, H, W, Cin, KH, KW, Cout, stride, pads) in enumerate(STREAMK_GEOMS):
+        rng = np.random.default_rng(300 + gi)
+        x = wl.integers(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+        f = wl.integers(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
+        ref, _ = oracle.conv2d(x, f, stride, pads)
+        dx, df = dev(x), dev(f)
+        gemm_path = KH == 1 and KW == 1 and stride == (1, 1) and pads == (0, 0, 0, 0)
+        for cfg in pk.configs():
+            if not cfg["streamk"] or (cfg["kind"] == 0) != gemm_path:
+                continue
+            outs = []
+            pk.force_config(cfg["name"])
+            try:
+                for _ in range(2):
+                    y = torch.full(ref.shape, float("nan"), dtype=torch.float32, device="cuda")
+                    pk.conv2d_fwd(dx, df, stride=stride, padding=pads, out=y)
+                    assert pk.last_config_name() == cfg["name"]
+                    outs.append(host(y))
+            finally:
+                pk.force_config(None)
+            assert np.array_equal(outs[0].astype(np.float64), ref), (cfg["name"], gi)
+            assert np.array_equal(outs[0], outs[1]), (cfg["name"], gi)
+            ran += 1
+    assert ran >= 8
+
+
+def test_streamk_needs_workspace():
+    """A forced stream-K configuration without room for its partial tiles
+    reports PK_ERR_WORKSPACE; the selector's own choices fall back."""
+    torch, pk = require_gpu()
+    x = torch.ones((1, 8, 8, 16), dtype=torch.float32, device="cuda")
+    f = torch.ones((3, 3, 16, 16), dtype=torch.float32, device="cuda")
+    y = torch.empty((1, 8, 8, 16), dtype=torch.float32, device="cuda")
+    name = next(c["name"] for c in pk.configs() if c["streamk"] and c["kind"] == 1)
+    pk.force_config(name)
+    try:
+        st = pk.binding.conv2d_fwd_raw(x.data_ptr(), 1, 8, 8, 16, f.data_ptr(), 3, 3, 16, 1, 1, 1, 1, 1, 1,
+                                       y.data_ptr(), 8, 8, None, 0)
+    finally:
+        pk.force_config(None)
+    assert st == 3

@@ -151,7 +151,9 @@ def test_gemm_sweep_sampled(case):
 def test_every_gemm_config_forced():
     torch, pk = require_gpu()
     for cfg in pk.configs():
-        if cfg["kind"] != 0:
+        # stream-K runs through the convolution call only; B-resident forms
+        # take only K == bk and N == bn (tested on their own)
+        if cfg["kind"] != 0 or cfg["streamk"] or cfg["bres"]:
             continue
         ta = "T" if cfg["trans_a"] else "N"
         tb = "T" if cfg["trans_b"] else "N"
@@ -221,3 +223,71 @@ def test_paper_gemm_sweep(case):
     out = host(dC)
     ref, scale = oracle.sgemm("N", "N", case.M, case.N, case.K, 1.0, A, case.lda, B, case.ldb, 0.0, C, case.ldc)
     assert_parity(out, ref, scale, case.name + " " + pk.last_config_name())
+
+
+def test_streamk_configs_refused_by_sgemm():
+    """Stream-K needs a workspace, which pk_sgemm does not take: a forced
+    stream-K configuration is refused with PK_ERR_NOT_SUPPORTED."""
+    torch, pk = require_gpu()
+    name = next(c["name"] for c in pk.configs() if c["streamk"] and c["kind"] == 0)
+    a = torch.ones((64, 64), dtype=torch.float32, device="cuda")
+    c = torch.zeros((64, 64), dtype=torch.float32, device="cuda")
+    pk.force_config(name)
+    try:
+        st = pk.binding.sgemm("N", "N", 64, 64, 64, 1.0, a.data_ptr(), 64, a.data_ptr(), 64, 0.0, c.data_ptr(), 64)
+    finally:
+        pk.force_config(None)
+    assert st == 2
+
+
+def test_bres_configs():
+    """B-resident streaming configurations: the 1x1 convolution path and
+    pk_sgemm with beta != 0 and leading-dimension slack, on row counts that
+    leave a ragged last tile and several tiles per work-group; integer data,
+    so every output must equal the oracle bit for bit; a product whose K or
+    N differs from the tile is refused."""
+    torch, pk = require_gpu()
+    ran = 0
+    for cfg in pk.configs():
+        if not cfg["bres"]:
+            continue
+        K, N = cfg["bk"], cfg["bn"]
+        for M in (cfg["bm"] * 3 + 5, 300 * cfg["bm"] + 17):
+            rng = np.random.default_rng(M + N)
+            A = wl.integers(rng, M * K).reshape(M, K)
+            B = wl.integers(rng, K * N).reshape(K, N)
+            # as a 1x1 convolution (image M x 1 x 1 pixels of K channels)
+            x = A.reshape(M, 1, 1, K)
+            f = B.reshape(1, 1, K, N)
+            y = torch.full((M, 1, 1, N), float("nan"), dtype=torch.float32, device="cuda")
+            pk.force_config(cfg["name"])
+            try:
+                pk.conv2d_fwd(dev(x), dev(f), padding="VALID", out=y)
+                assert pk.last_config_name() == cfg["name"]
+            finally:
+                pk.force_config(None)
+            ref, _ = oracle.sgemm("N", "N", M, N, K, 1.0, A, K, B, N, 0.0, None, N)
+            assert np.array_equal(host(y).reshape(M, N).astype(np.float64), ref), cfg["name"]
+            ran += 1
+        # pk_sgemm, beta = 0.5, lda / ldb / ldc with slack (the slack of C untouched)
+        M = 5 * cfg["bm"] + 3
+        rng = np.random.default_rng(7 * N)
+        A = wl.integers(rng, M * (K + 8)).reshape(M, K + 8)
+        B = wl.integers(rng, K * (N + 4)).reshape(K, N + 4)
+        C = wl.integers(rng, M * (N + 12)).reshape(M, N + 12)
+        dA, dB, dC = dev(A), dev(B), dev(C)  # held: a freed temporary's memory is handed out again
+        pk.force_config(cfg["name"])
+        try:
+            st = pk.binding.sgemm("N", "N", M, N, K, 1.0, dA.data_ptr(), K + 8, dB.data_ptr(), N + 4, 0.5,
+                                  dC.data_ptr(), N + 12)
+            torch.cuda.synchronize()
+            st_bad = pk.binding.sgemm("N", "N", M, N, K // 2, 1.0, dA.data_ptr(), K + 8, dB.data_ptr(),
+                                      N + 4, 0.5, dC.data_ptr(), N + 12)
+        finally:
+            pk.force_config(None)
+        assert st == 0 and st_bad == 2
+        out = host(dC)
+        ref, _ = oracle.sgemm("N", "N", M, N, K, 1.0, A, K + 8, B, N + 4, 0.5, C, N + 12)
+        assert np.array_equal(out[:, :N].astype(np.float64), ref), cfg["name"]
+        assert np.array_equal(out[:, N:], C[:, N:]), cfg["name"]
+    assert ran >= 8

@@ -71,7 +71,7 @@ def test_winograd_every_product_config_forced():
     ref_s, _ = oracle.conv2d(xs, fs, (1, 1), (1, 1, 1, 1))
     ran = 0
     for cfg in pk.configs():
-        if cfg["kind"] != 0 or cfg["trans_a"] or cfg["trans_b"] or cfg["persistent"]:
+        if cfg["kind"] != 0 or cfg["trans_a"] or cfg["trans_b"] or cfg["persistent"] or cfg["streamk"] or cfg["bres"]:
             continue
         out, used = _run(pk, x, f, (1, 1, 1, 1), force=cfg["name"])
         assert used == cfg["name"]
