@@ -578,7 +578,7 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
     TunedShape tbuf;
     if (!c) {
         tuned = (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
-        const bool direct_ok = !gemm_path && pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535;
+        const bool direct_ok = !gemm_path && pk::direct_conv_fits(nullptr, W, Wo, Cout, KH, KW, Cin, sh, sw) && N <= 65535;
         if (direct_ok && !(tuned && v4)) return 0;
         c = (tuned && v4) ? find_config(tuned->config) : nullptr;
         if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
@@ -675,15 +675,27 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     } else {
-        const bool direct_ok = pk::direct_conv_fits(KH, KW, Cin, sh, sw) && N <= 65535;
+        auto direct_ok = [&](const Config *d) {
+            return N <= 65535 && pk::direct_conv_fits(d, W, Wo, Cout, KH, KW, Cin, sh, sw);
+        };
         if (c) {
             if (!conv_config_fits(c, va4, vb4)) return PK_ERR_NOT_SUPPORTED;
-            if (c->kind == pk::KIND_DIRECT && !direct_ok) return PK_ERR_NOT_SUPPORTED;
+            if (c->kind == pk::KIND_DIRECT && !direct_ok(c)) return PK_ERR_NOT_SUPPORTED;
         } else {
-            // a measured choice first (it may name the direct kernel), then the rules
+            // a measured choice first (it may name the direct kernel), then the
+            // rules: the persistent direct form when its patch fits, else the
+            // one-tile-per-work-group form
             c = tuned ? find_config(tuned->config) : nullptr;
-            if (c && (!conv_config_fits(c, va4, vb4) || (c->kind == pk::KIND_DIRECT && !direct_ok))) c = nullptr;
-            if (!c && direct_ok) c = find_config("direct_8x32x64_k32");
+            if (c && (!conv_config_fits(c, va4, vb4) || (c->kind == pk::KIND_DIRECT && !direct_ok(c)))) c = nullptr;
+            if (!c) {
+                for (const char *name : {"direct_8x32x64_k32_p", "direct_8x32x64_k32"}) {
+                    const Config *d = find_config(name);
+                    if (d && direct_ok(d)) {
+                        c = d;
+                        break;
+                    }
+                }
+            }
             if (!c) c = select_conv(M, Cout, va4, vb4);
         }
         if (!c) return PK_ERR_NOT_SUPPORTED;

@@ -46,8 +46,10 @@ hipError_t launch_splitk_reduce(const float *ws, float *C, int M, int N, int64_t
 int device_cu_count();
 
 // Whether the tiled direct convolution takes this window (short reduction,
-// input patch fits its LDS buffer).
-bool direct_conv_fits(int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t sw);
+// input patch fits its LDS buffer): configuration c, or any direct
+// configuration when c is NULL.
+bool direct_conv_fits(const Config *c, int64_t W, int64_t Wo, int64_t Cout, int64_t KH, int64_t KW, int64_t Cin,
+                      int64_t sh, int64_t sw);
 
 hipError_t launch_scale(float *C, int M, int N, int64_t ldc, float beta, hipStream_t stream);
 // p[0 .. n) = 0 (a kernel, so that it may be captured in a graph).

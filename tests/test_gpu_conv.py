@@ -106,23 +106,85 @@ DIRECT_GEOMS = [
 ]
 
 
+DIRECT_CONFIGS = ["direct_8x32x64_k32", "direct_8x32x64_k32_p"]
+
+
+def _direct_patch_floats(KH, KW, Cin, stride):
+    return (7 * stride[0] + KH) * (31 * stride[1] + KW) * Cin
+
+
+@pytest.mark.parametrize("name", DIRECT_CONFIGS)
 @pytest.mark.parametrize("geom", DIRECT_GEOMS, ids=lambda g: "x".join(map(str, g[:7])) + "_s%d%d" % g[7])
-def test_direct_conv_geometries(geom):
+def test_direct_conv_geometries(geom, name):
     torch, pk = require_gpu()
     N, H, W, Cin, KH, KW, Cout, stride, pads = geom
     rng = np.random.default_rng(sum(geom[:7]) + 1)
     x = wl.uniform(rng, N * H * W * Cin).reshape(N, H, W, Cin)
     f = wl.uniform(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
-    out, cfg = _run(pk, x, f, stride, pads)
-    assert cfg.startswith("direct"), cfg
+    if name.endswith("_p") and _direct_patch_floats(KH, KW, Cin, stride) > 2048:
+        # the persistent form stages at most 2048 patch floats: a forced call is refused
+        with pytest.raises(pk.PkError):
+            _run(pk, x, f, stride, pads, force=name)
+        return
+    out, cfg = _run(pk, x, f, stride, pads, force=name)
+    assert cfg == name
     ref, scale = oracle.conv2d(x, f, stride, pads)
     assert out.shape == ref.shape
     assert_parity(out, ref, scale, str(geom) + " " + cfg)
     xi = wl.integers(rng, x.size).reshape(x.shape)
     fi = wl.integers(rng, f.size).reshape(f.shape)
-    out, cfg = _run(pk, xi, fi, stride, pads)
+    out, cfg = _run(pk, xi, fi, stride, pads, force=name)
     ref, _ = oracle.conv2d(xi, fi, stride, pads)
     assert np.array_equal(out.astype(np.float64), ref), (geom, cfg)
+
+
+def test_direct_conv_default_choice():
+    """The selector takes the persistent direct form where its patch fits and
+    the one-tile-per-work-group form otherwise."""
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(5)
+    for geom, want in [((1, 9, 40, 3, 3, 3, 16, (1, 1), (1, 1, 1, 1)), "direct_8x32x64_k32_p"),
+                       ((1, 40, 40, 2, 4, 4, 32, (3, 3), (0, 0, 0, 0)), "direct_8x32x64_k32")]:
+        N, H, W, Cin, KH, KW, Cout, stride, pads = geom
+        x = wl.integers(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+        f = wl.integers(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
+        out, cfg = _run(pk, x, f, stride, pads)
+        assert cfg == want, (geom, cfg)
+        ref, _ = oracle.conv2d(x, f, stride, pads)
+        assert np.array_equal(out.astype(np.float64), ref), (geom, cfg)
+
+
+# Enough tiles that every resident work-group of the persistent direct form
+# walks several, with channel-block changes inside a work-group's run (Cout =
+# 130: three blocks of 64) and both patch sizes (4 and 8 floats per thread).
+DIRECT_LOOP_GEOMS = [
+    (32, 56, 56, 3, 3, 3, 130, (1, 1), (1, 1, 1, 1)),
+    (96, 64, 70, 3, 3, 3, 64, (1, 2), (1, 1, 1, 1)),
+    (8, 224, 224, 3, 3, 3, 64, (1, 1), (1, 1, 1, 1)),
+]
+
+
+@pytest.mark.parametrize("geom", DIRECT_LOOP_GEOMS, ids=lambda g: "x".join(map(str, g[:7])) + "_s%d%d" % g[7])
+def test_direct_persistent_loops_over_tiles(geom):
+    torch, pk = require_gpu()
+    N, H, W, Cin, KH, KW, Cout, stride, pads = geom
+    rng = np.random.default_rng(sum(geom[:7]) + 7)
+    x = wl.integers(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+    f = wl.integers(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
+    Ho, Wo = oracle.conv2d_out_dims(H, W, KH, KW, *stride, *pads)
+    y = torch.full((N, Ho, Wo, Cout), float("nan"), dtype=torch.float32, device="cuda")
+    pk.force_config("direct_8x32x64_k32_p")
+    try:
+        pk.conv2d_fwd(dev(x), dev(f), stride=stride, padding=pads, out=y)
+        used = pk.last_config_name()
+    finally:
+        pk.force_config(None)
+    assert used == "direct_8x32x64_k32_p"
+    out = host(y)
+    assert np.all(np.isfinite(out))
+    idx = sample_conv_outputs(N, Ho, Wo, Cout, 6000, sum(geom[:7]))
+    ref, _ = oracle.conv2d_at(x, f, stride, pads, idx)
+    assert np.array_equal(out.reshape(-1)[idx].astype(np.float64), ref)
 
 
 @pytest.mark.parametrize("splits", [2, 3, 5])
