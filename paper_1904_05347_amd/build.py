@@ -19,7 +19,7 @@ ARCH = os.environ.get("PK_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = [
-    "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
+    "--offload-arch=" + ARCH, "-O3", "-std=c++20", "-fPIC",
     # code object v5: loadable by the HIP runtime that PyTorch ships as well
     "-mcode-object-version=5",
     "-Wall", "-Wno-unused-result", "-Rpass-analysis=kernel-resource-usage",

@@ -164,7 +164,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},
     {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x64_w2x4_v44_o2", 1},
     {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
-    {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
+    {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},
     {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 6},
     {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 1},
 };
@@ -242,8 +242,14 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, bool 
     return find_config(name);
 }
 
-// A B-resident configuration runs only the product its LDS holds whole.
-bool bres_fits(const Config *c, int64_t N, int64_t K) { return !c->bres || (N == c->bn && K == c->bk); }
+// A B-resident configuration runs only products whose K is its one K-block
+// and whose N is a multiple of its column block.
+// (Its C stores address a tile's rows in 32 bits: (BM + 1) rows of ldc floats.)
+bool bres_fits(const Config *c, int64_t N, int64_t K, int64_t ldc)
+{
+    return !c->bres || (N % c->bn == 0 && K == c->bk &&
+                        (int64_t)(c->bm + 1) * ldc * (int64_t)sizeof(float) < ((int64_t)1 << 31));
+}
 
 bool conv_config_fits(const Config *c, bool va4, bool vb4)
 {
@@ -530,12 +536,12 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float al
     if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
     if (c) {
         // stream-K needs a workspace, which this call does not take
-        if (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K)) return PK_ERR_NOT_SUPPORTED;
+        if (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K, ldc)) return PK_ERR_NOT_SUPPORTED;
     } else {
         TunedShape tbuf;
         const TunedShape *t = find_tuned(0, ta, tb, M, N, K, 0, 0, &tbuf) ? &tbuf : nullptr;
         c = t ? find_config(t->config) : nullptr;
-        if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K))) c = nullptr;
+        if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K, ldc))) c = nullptr;
         if (!c) c = select_gemm(ta, tb, M, N, K, vec_ok);
         if (!c) return PK_ERR_NOT_SUPPORTED;
     }
@@ -667,10 +673,10 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     const bool vb4 = Cout % 4 == 0 && aligned16(f);
     if (gemm_path) {
         if (c) {
-            if (!gemm_config_fits(c, 0, 0, vec_ok) || !bres_fits(c, Cout, Cin)) return PK_ERR_NOT_SUPPORTED;
+            if (!gemm_config_fits(c, 0, 0, vec_ok) || !bres_fits(c, Cout, Cin, Cout)) return PK_ERR_NOT_SUPPORTED;
         } else {
             c = (tuned && vec_ok) ? find_config(tuned->config) : nullptr;
-            if (c && !bres_fits(c, Cout, Cin)) c = nullptr;
+            if (c && !bres_fits(c, Cout, Cin, Cout)) c = nullptr;
             if (!c) c = select_gemm(0, 0, M, Cout, Cin, vec_ok);
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }

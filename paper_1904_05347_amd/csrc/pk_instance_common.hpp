@@ -99,12 +99,13 @@ static hipError_t launch_gemm_streamk(const KernelArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
-// B-resident streaming launch: as many work-groups as the CUs hold (at most
-// one per BM-row tile), each walking a contiguous range of tiles.
+// B-resident streaming launch: as many work-groups as the CUs hold, a
+// multiple of (XCD count) x (column blocks N / BN), each walking a contiguous
+// range of row tiles of one column block.
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int OCC>
 static hipError_t launch_gemm_bres(const KernelArgs &a, hipStream_t stream)
 {
-    if (a.K != BK || a.N != BN || a.splits > 1 || a.nbatch > 1) return hipErrorInvalidValue;
+    if (a.K != BK || a.N % BN != 0 || a.N < BN || a.splits > 1 || a.nbatch > 1) return hipErrorInvalidValue;
     const bool beta = reads_c<A_KCONTIG>(a);
     auto kernel = beta ? gemm_bres_kernel<BM, BN, BK, WAVES_M, WAVES_N, OCC, true>
                        : gemm_bres_kernel<BM, BN, BK, WAVES_M, WAVES_N, OCC, false>;
@@ -116,9 +117,14 @@ static hipError_t launch_gemm_bres(const KernelArgs &a, hipStream_t stream)
         per_cu[beta] = n;
     }
     const int64_t tiles = (a.M + BM - 1) / BM;
-    int64_t grid = (int64_t)per_cu[beta] * device_cu_count();
-    if (grid > tiles) grid = tiles;
-    hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(threads), 0, stream, a);
+    const int64_t ncb = a.N / BN;
+    const int64_t x = a.xcds > 1 ? a.xcds : 1;
+    // row groups per column block: a multiple of x, at most one per tile (and x)
+    int64_t groups = (int64_t)per_cu[beta] * device_cu_count() / ncb;
+    groups -= groups % x;
+    if (groups > tiles) groups = (tiles + x - 1) / x * x;
+    if (groups < x) groups = x;
+    hipLaunchKernelGGL(kernel, dim3((unsigned)(groups * ncb)), dim3(threads), 0, stream, a);
     return hipGetLastError();
 }
 

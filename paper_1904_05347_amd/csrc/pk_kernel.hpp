@@ -34,6 +34,7 @@
 #include <stdint.h>
 
 #include <type_traits>
+#include <utility>
 
 #include "pk_args.hpp"
 
@@ -998,20 +999,30 @@ gemm_streamk_kernel(KernelArgs p)
 // convolutions of ResNet-50's bottlenecks: K = 64 input channels, N = 64 or
 // 256 output channels).  There the whole of B is one K-block and at most
 // 64 KB, while A and C stream through HBM once (8-16 flop per byte), so the
-// time goes to memory, not to the MFMAs.  A persistent work-group loads B
-// once (stored n-major, k contiguous, for 16-byte operand reads), then walks
-// a contiguous range of BM-row tiles of A: the next tile's rows are loaded
-// into registers while the current one is multiplied, and the current tile's
-// C stores drain while the next one computes.  K == BK and N == BN exactly
-// (the launcher checks); M is arbitrary.
+// time goes to memory, not to the MFMAs.  A persistent work-group loads one
+// BN-column block of B once (stored n-major, k contiguous, for 16-byte
+// operand reads), then walks a contiguous range of BM-row tiles of A.
+// K == BK and N a multiple of BN (the launcher checks); M is arbitrary.
+//
+// Per tile t the A rows of tile t+2 are fetched into registers before tile
+// t's C stores are issued, and stored to LDS only after tile t+1 has been
+// multiplied.  The vector-memory counter orders loads and stores together,
+// so that wait covers the loads alone, never the stores behind them: tile t's
+// stores drain while tile t+1 multiplies.  For that count to be exact on
+// every path nothing around the loads and stores is conditional: rows past M
+// are fetched from row M-1 and zeroed on their way into LDS, and C is written
+// with buffer stores whose out-of-range offset (rows past M) the hardware
+// drops.  (beta != 0 keeps the generic epilogue, which reads C.)
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int OCC, bool BETA>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 gemm_bres_kernel(KernelArgs p)
 {
     typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, true, 4, 4> G;
-    typedef typename G::ALoader ALoader;
     constexpr int NT = G::NT;
+    constexpr int CPR = BK / 4;              // 16-byte chunks per A row
+    constexpr int AL = BM * BK / (4 * NT);   // A chunks per thread per tile
     static_assert(BN % 4 == 0 && (BK * BN / 4) % NT == 0, "B staging");
+    static_assert(NT % CPR == 0 && AL >= 1 && AL <= 32 && (BM * BK) % (4 * NT) == 0, "A staging");
 
     __shared__ __attribute__((aligned(16))) float smem[2 * G::A_STAGE + G::B_STAGE];
     float *As = smem;                   // [2][BM][BK + PAD]
@@ -1023,9 +1034,19 @@ gemm_bres_kernel(KernelArgs p)
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int l32 = lane & 31, h = lane >> 5;
 
+    // N = NCB column blocks of BN, each served by gridDim.x / NCB work-groups.
+    // Work-group b serves block (b / X) % NCB (X = XCD count, a divisor of the
+    // grid per block): the work-groups that walk the same rows for the other
+    // blocks run on the same XCD, so A is fetched into its L2 once.
+    const int ncb = p.N / BN;
+    const int X = p.xcds > 1 ? p.xcds : 1;
+    const int cb = (int)(blockIdx.x / X) % ncb;
+    const int rg = (int)(blockIdx.x / (X * ncb)) * X + (int)(blockIdx.x % X);
+    const int groups = (int)gridDim.x / ncb;
+    const int n0 = cb * BN;
     const int tiles = (p.M + BM - 1) / BM;
-    const int t0 = (int)(((int64_t)blockIdx.x * tiles) / gridDim.x);
-    const int t1 = (int)(((int64_t)(blockIdx.x + 1) * tiles) / gridDim.x);
+    const int t0 = (int)(((int64_t)rg * tiles) / groups);
+    const int t1 = (int)(((int64_t)(rg + 1) * tiles) / groups);
     if (t0 >= t1) return;  // uniform over the work-group, before any barrier
 
     // B: BK x BN row-major in global memory -> Bs[n][k]
@@ -1033,52 +1054,144 @@ gemm_bres_kernel(KernelArgs p)
     for (int i = 0; i < BK * BN / 4 / NT; ++i) {
         const int c = tid + i * NT;
         const int k = c / (BN / 4), n = (c % (BN / 4)) * 4;
-        const f32x4 v = *reinterpret_cast<const f32x4 *>(p.B + (int64_t)k * p.ldb + n);
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(p.B + (int64_t)k * p.ldb + n0 + n);
         Bs[(n + 0) * G::LDB_S + k] = v[0];
         Bs[(n + 1) * G::LDB_S + k] = v[1];
         Bs[(n + 2) * G::LDB_S + k] = v[2];
         Bs[(n + 3) * G::LDB_S + k] = v[3];
     }
-    ALoader la;
-    typename ALoader::VT ra[ALoader::LOADS];
-    la.init(p.A, p.lda, t0 * BM, p.M, 0, tid);
-    la.load(ra, 0, p.K);
-    la.template store<G::LDA_S>(As, ra, tid);
+
+    // this thread's A chunks: row (tid + i*NT) / CPR of the tile, columns col .. col+3
+    const int col = (tid % CPR) * 4;
+    f32x4 ra[AL];
+    unsigned inside = 0;  // bit i: chunk i's row is below M
+    auto load_a = [&](int t) {
+        inside = 0;
+#pragma unroll
+        for (int i = 0; i < AL; ++i) {
+            const int row = t * BM + (tid + i * NT) / CPR;
+            const bool ok = row < p.M;
+            ra[i] = *reinterpret_cast<const f32x4 *>(p.A + (int64_t)(ok ? row : p.M - 1) * p.lda + col);
+            inside |= (unsigned)ok << i;
+        }
+    };
+    auto write_a = [&](float *stage) {
+#pragma unroll
+        for (int i = 0; i < AL; ++i) {
+            const f32x4 v = ((inside >> i) & 1u) ? ra[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+            *reinterpret_cast<f32x4 *>(stage + ((tid + i * NT) / CPR) * G::LDA_S + col) = v;
+        }
+    };
+
+    load_a(t0);
+    write_a(As);
+    if (t0 + 1 < t1) load_a(t0 + 1);
+    // nothing of the set-up stays in flight into the loop: the loop then only
+    // ever waits for the loads it issued itself, which precede its stores
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
     const int a_row = wm * G::WM + l32;
     const int b_row = wn * G::WN + l32;
-    typename G::Acc acc;
-    G::zero(acc);
     typename G::FragA fa[2];
     typename G::FragB fb[2];
     constexpr int NGR = G::NG;
-    int stage = 0;
-    G::read_group(As, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
+    // C(t*BM + wm*WM + 4h + i*32 + 8*(r/4) + r%4, wn*WN + l32 + 32j) = acc[i][j][r]: a
+    // wave-uniform part plus this lane's offset
+    const unsigned c_lane = 4u * (unsigned)h * (unsigned)p.ldc + (unsigned)(n0 + wn * G::WN + l32);
+    const float alpha = p.alpha;
 
-    for (int t = t0; t < t1; ++t) {
-        const bool more = t + 1 < t1;
-        if (more) {
-            la.init(p.A, p.lda, (t + 1) * BM, p.M, 0, tid);
-            la.load(ra, 0, p.K);
-        }
-        const float *as = As + stage * G::A_STAGE;
+    // Stores q = [Q0, Q1) of tile t's results: q = (i*16 + r)*RN + j.
+    constexpr int NQ = G::RM * 16 * G::RN;
+    auto store_range = [&](const typename G::Acc &acc, int t, auto q0_c, auto q1_c) {
+        constexpr int Q0 = decltype(q0_c)::value, Q1 = decltype(q1_c)::value;
+        const __amdgpu_buffer_rsrc_t cres =
+            __builtin_amdgcn_make_buffer_rsrc(p.C + (int64_t)t * BM * p.ldc, (short)0, 0x7fffffff, 0x00020000);
 #pragma unroll
-        for (int g = 0; g < NGR - 1; ++g) {
-            G::read_group(as, Bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
-            __builtin_amdgcn_sched_barrier(0);
-            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        for (int q = Q0; q < Q1; ++q) {
+            const int j = q % G::RN, r = (q / G::RN) % 16, i = q / (16 * G::RN);
+            const int dr = wm * G::WM + i * 32 + 8 * (r >> 2) + (r & 3);  // row in the tile, less 4h
+            const bool ok = t * BM + dr + 4 * h < p.M;
+            const unsigned e = (unsigned)(dr * p.ldc + 32 * j) + c_lane;
+            // the builtin's data operand is a 32-bit integer: pass the float's bits
+            const float val = alpha * acc[i][j][r];
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, val), cres, ok ? 4u * e : 0x80000000u,
+                                                  0, 0);
         }
-        if (more) la.template store<G::LDA_S>(As + (stage ^ 1) * G::A_STAGE, ra, tid);
-        __syncthreads();
-        // unconditional, as in gemm_kernel (after the last tile it reads a
-        // stage that is never used)
-        G::read_group(As + (stage ^ 1) * G::A_STAGE, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
-        __builtin_amdgcn_sched_barrier(0);
-        G::mma_group(acc, fa[(NGR - 1) & 1], fb[(NGR - 1) & 1]);
-        G::template store<BETA>(p, acc, t * BM + wm * G::WM + 4 * h, wn * G::WN + l32, 0);
+    };
+    // The MFMAs of one tile (A from stage `as`) into acc; with PREV, the
+    // stores of the previous tile's results (prev) are issued in slices
+    // between the MFMA groups, so no wave ever waits at a barrier or issues
+    // its stores while its SIMD's matrix pipe has nothing to do.
+    auto mma_tile = [&](const float *as, typename G::Acc &acc, const typename G::Acc &prev, int tprev, auto with_prev) {
+        constexpr bool PREV = decltype(with_prev)::value;
+        G::read_group(as, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
         G::zero(acc);
-        stage ^= 1;
+        constexpr int SPG = (NQ + NGR - 1) / NGR;  // stores per group
+        [&]<int... G_>(std::integer_sequence<int, G_...>) {
+            (
+                [&] {
+                    constexpr int g = G_;
+                    if (g + 1 < NGR) G::read_group(as, Bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    G::mma_group(acc, fa[g & 1], fb[g & 1]);
+                    if constexpr (PREV) {
+                        constexpr int q0 = g * SPG < NQ ? g * SPG : NQ;
+                        constexpr int q1 = (g + 1) * SPG < NQ ? (g + 1) * SPG : NQ;
+                        store_range(prev, tprev, std::integral_constant<int, q0>{}, std::integral_constant<int, q1>{});
+                    }
+                }(),
+                ...);
+        }(std::make_integer_sequence<int, NGR>{});
+    };
+    auto store_all = [&](const typename G::Acc &acc, int t) {
+        if constexpr (BETA)
+            G::template store<true>(p, acc, t * BM + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, 0);
+        else
+            store_range(acc, t, std::integral_constant<int, 0>{}, std::integral_constant<int, NQ>{});
+    };
+    // After tile t: its successor's A rows into the other stage, the barrier
+    // that also ends every wave's reads of tile t's stage, then the loads of
+    // tile t+2 (issued before any store of tile t).
+    auto advance = [&](int t, int stage) {
+        if (t + 1 < t1) write_a(As + (stage ^ 1) * G::A_STAGE);
+        __syncthreads();
+        if (t + 2 < t1) load_a(t + 2);
+    };
+
+    typename G::Acc acc0, acc1;
+    if constexpr (BETA) {
+        // beta != 0 reads C in its epilogue: tiles one after the other
+        int stage = 0;
+        for (int t = t0; t < t1; ++t) {
+            mma_tile(As + stage * G::A_STAGE, acc0, acc1, 0, std::false_type{});
+            advance(t, stage);
+            store_all(acc0, t);
+            stage ^= 1;
+        }
+    } else {
+        mma_tile(As, acc0, acc1, 0, std::false_type{});
+        advance(t0, 0);
+        int t = t0 + 1, stage = 1;
+        // tiles in pairs so that each accumulator set has a fixed name
+        for (;;) {
+            if (t >= t1) {
+                store_all(acc0, t - 1);
+                break;
+            }
+            mma_tile(As + stage * G::A_STAGE, acc1, acc0, t - 1, std::true_type{});
+            advance(t, stage);
+            ++t;
+            stage ^= 1;
+            if (t >= t1) {
+                store_all(acc1, t - 1);
+                break;
+            }
+            mma_tile(As + stage * G::A_STAGE, acc0, acc1, t - 1, std::true_type{});
+            advance(t, stage);
+            ++t;
+            stage ^= 1;
+        }
     }
 }
 

@@ -243,16 +243,18 @@ def test_streamk_configs_refused_by_sgemm():
 def test_bres_configs():
     """B-resident streaming configurations: the 1x1 convolution path and
     pk_sgemm with beta != 0 and leading-dimension slack, on row counts that
-    leave a ragged last tile and several tiles per work-group; integer data,
-    so every output must equal the oracle bit for bit; a product whose K or
-    N differs from the tile is refused."""
+    leave a ragged last tile and several tiles per work-group, with N one,
+    two and four column blocks; integer data, so every output must equal the
+    oracle bit for bit; a product whose K differs from the K-block or whose N
+    is not a multiple of the column block is refused."""
     torch, pk = require_gpu()
     ran = 0
     for cfg in pk.configs():
         if not cfg["bres"]:
             continue
-        K, N = cfg["bk"], cfg["bn"]
-        for M in (cfg["bm"] * 3 + 5, 300 * cfg["bm"] + 17):
+        K = cfg["bk"]
+        for M, N in ((cfg["bm"] * 3 + 5, cfg["bn"]), (300 * cfg["bm"] + 17, cfg["bn"]),
+                     (40 * cfg["bm"] + 9, 2 * cfg["bn"]), (300 * cfg["bm"] + 3, 4 * cfg["bn"])):
             rng = np.random.default_rng(M + N)
             A = wl.integers(rng, M * K).reshape(M, K)
             B = wl.integers(rng, K * N).reshape(K, N)
@@ -270,7 +272,7 @@ def test_bres_configs():
             assert np.array_equal(host(y).reshape(M, N).astype(np.float64), ref), cfg["name"]
             ran += 1
         # pk_sgemm, beta = 0.5, lda / ldb / ldc with slack (the slack of C untouched)
-        M = 5 * cfg["bm"] + 3
+        M, N = 5 * cfg["bm"] + 3, 2 * cfg["bn"]
         rng = np.random.default_rng(7 * N)
         A = wl.integers(rng, M * (K + 8)).reshape(M, K + 8)
         B = wl.integers(rng, K * (N + 4)).reshape(K, N + 4)
@@ -283,11 +285,13 @@ def test_bres_configs():
             torch.cuda.synchronize()
             st_bad = pk.binding.sgemm("N", "N", M, N, K // 2, 1.0, dA.data_ptr(), K + 8, dB.data_ptr(),
                                       N + 4, 0.5, dC.data_ptr(), N + 12)
+            st_bad_n = pk.binding.sgemm("N", "N", M, N - 4, K, 1.0, dA.data_ptr(), K + 8, dB.data_ptr(),
+                                        N + 4, 0.5, dC.data_ptr(), N + 12)
         finally:
             pk.force_config(None)
-        assert st == 0 and st_bad == 2
+        assert st == 0 and st_bad == 2 and st_bad_n == 2
         out = host(dC)
         ref, _ = oracle.sgemm("N", "N", M, N, K, 1.0, A, K + 8, B, N + 4, 0.5, C, N + 12)
         assert np.array_equal(out[:, :N].astype(np.float64), ref), cfg["name"]
         assert np.array_equal(out[:, N:], C[:, N:]), cfg["name"]
-    assert ran >= 8
+    assert ran >= 16
