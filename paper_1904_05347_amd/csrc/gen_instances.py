@@ -62,6 +62,11 @@ NN_SHORT_K = [(64, 64, 64, 2, 2, 4, 4, 1), (128, 64, 64, 2, 2, 4, 4, 1), (64, 25
               (128, 256, 32, 2, 4, 4, 4, 2)]
 NN_SHORT_K_1S = [(64, 64, 64, 2, 2, 4, 4, 1), (128, 64, 64, 2, 2, 4, 4, 1), (128, 128, 64, 2, 4, 4, 4, 2)]
 
+# Loads two K-blocks ahead ("_d2"): small tiles whose K-block is too short
+# to cover the global-load latency (NN GEMM and convolution).
+DEEP = [(64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 32, 2, 2, 4, 4, 1), (128, 64, 32, 2, 2, 4, 4, 1),
+        (64, 128, 32, 2, 2, 4, 4, 1), (128, 128, 32, 2, 4, 4, 4, 2)]
+
 # TT only needs a large, a small and a scalar-load tile.
 TT_TILES = [(128, 128, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 1, 1, 1)]
 
@@ -84,7 +89,7 @@ CONV_TILES = [
 ]
 
 
-def _name(kind, t, layout=None, persistent=False, single=False, streamk=False):
+def _name(kind, t, layout=None, persistent=False, single=False, streamk=False, deep=False):
     bm, bn, bk, wm, wn, va, vb, occ = t
     s = "%s_%dx%dx%d_w%dx%d" % (kind, bm, bn, bk, wm, wn)
     if layout:
@@ -98,6 +103,8 @@ def _name(kind, t, layout=None, persistent=False, single=False, streamk=False):
         s += "_s1"
     if streamk:
         s += "_sk"
+    if deep:
+        s += "_d2"
     return s
 
 
@@ -153,6 +160,10 @@ def main():
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
                            % (_name("gemm", t, layout), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
+        for t in (DEEP if layout == "nn" else []):
+            bm, bn, bk, wm, wn, va, vb, occ = t
+            entries.append("PK_GEMM_D(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
+                           % (_name("gemm", t, layout, deep=True), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
         for t in (SINGLE_STAGE + NN_SHORT_K_1S if layout == "nn" else []):
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM_1S(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
@@ -168,6 +179,10 @@ def main():
         bm, bn, bk, wm, wn, va, vb, occ = t
         entries.append("PK_CONV_P(%s, %d, %d, %d, %d, %d, %d, %d, %d)"
                        % (_name("conv", t, None, True), bm, bn, bk, wm, wn, va, vb, occ))
+    for t in DEEP:
+        bm, bn, bk, wm, wn, va, vb, occ = t
+        entries.append("PK_CONV_D(%s, %d, %d, %d, %d, %d, %d, %d, %d)"
+                       % (_name("conv", t, deep=True), bm, bn, bk, wm, wn, va, vb, occ))
     for t in CONV_STREAMK:
         bm, bn, bk, wm, wn, va, vb, occ = t
         entries.append("PK_CONV_SK(%s, %d, %d, %d, %d, %d, %d, %d, %d)"

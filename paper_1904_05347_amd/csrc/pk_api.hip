@@ -162,7 +162,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
     // ResNet-50 bottleneck layers at batch 32
     {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},
-    {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x64_w2x4_v44_o2", 1},
+    {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x32_w2x4_v44_o2_d2", 1},
     {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
     {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},
     {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 6},

@@ -128,6 +128,24 @@ static hipError_t launch_gemm_bres(const KernelArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
+// Loads two K-blocks ahead (same grid as launch_gemm).
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
+static hipError_t launch_gemm_deep(const KernelArgs &a, hipStream_t stream)
+{
+    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
+    const dim3 block(64 * WAVES_M * WAVES_N);
+    if constexpr (AMODE != A_CONV) {
+        if (reads_c<AMODE>(a)) {
+            hipLaunchKernelGGL((gemm_deep_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, true>),
+                               grid, block, 0, stream, a);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((gemm_deep_kernel<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB, OCC, false>), grid,
+                       block, 0, stream, a);
+    return hipGetLastError();
+}
+
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
 static hipError_t launch_gemm_single_stage(const KernelArgs &a, hipStream_t stream)
 {
@@ -171,6 +189,16 @@ static constexpr int lds_bytes()
     {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC, 0,                                    \
      lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>() / 2,            \
      &launch_gemm_single_stage<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>, 1}
+
+#define PK_GEMM_D(name, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC)                                       \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC, 0,                                    \
+     lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),                \
+     &launch_gemm_deep<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>}
+
+#define PK_CONV_D(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                               \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 0,                                      \
+     lds_bytes<BM, BN, BK, WM, WN, A_CONV, false, VA, VB>(),                                          \
+     &launch_gemm_deep<BM, BN, BK, WM, WN, A_CONV, false, VA, VB, OCC>}
 
 #define PK_CONV_P(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                               \
     {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 1,                                      \

@@ -564,6 +564,111 @@ gemm_kernel(KernelArgs p)
     G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
 }
 
+// The same contraction with the global loads TWO K-blocks ahead: two
+// register sets alternate, so the loads of block kb+2 are issued while block
+// kb multiplies and are stored to LDS only at the end of block kb+1.  Each
+// load then has two blocks' MFMAs to arrive in instead of one -- what a small
+// tile with a short K-block (64 x 64 x 32: about a thousand MFMA cycles per
+// wave) needs to cover the global-load latency when only a few work-groups
+// share a CU.  Same LDS stages, barrier and group pipeline as gemm_kernel.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC, bool BETA>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_deep_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
+    typedef typename G::ALoader ALoader;
+    typedef typename G::BLoader BLoader;
+
+    __shared__ __attribute__((aligned(16))) float smem[G::LDS_FLOATS];
+    float *As = smem;                      // [2][A_STAGE]
+    float *Bs = smem + 2 * G::A_STAGE;     // [2][B_STAGE]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+
+    if constexpr (AMODE != A_CONV) {  // product blockIdx.y of a batch
+        const int64_t bz = blockIdx.y;
+        p.A += bz * p.stride_a;
+        p.B += bz * p.stride_b;
+        p.C += bz * p.stride_c;
+    }
+    int tm, tn;
+    tile_coords(p, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    int kbeg, kend;
+    split_range(p, BK, blockIdx.z, kbeg, kend);
+
+    ALoader la;
+    BLoader lb;
+    if constexpr (AMODE == A_CONV)
+        la.init(p, m0, kbeg, tid);
+    else
+        la.init(p.A, p.lda, m0, p.M, kbeg, tid);
+    lb.init(p.B, p.ldb, n0, p.N, kbeg, tid);
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename ALoader::VT ra0[ALoader::LOADS], ra1[ALoader::LOADS];
+    typename BLoader::VT rb0[BLoader::LOADS], rb1[BLoader::LOADS];
+
+    auto fetch = [&](typename ALoader::VT *ra, typename BLoader::VT *rb, int kb) {
+        la.load(ra, kb * BK, p.K);
+        lb.load(rb, kb * BK, p.K);
+        la.advance();
+        lb.advance();
+    };
+    if (kbeg < kend) fetch(ra0, rb0, kbeg);
+    if (kbeg + 1 < kend) fetch(ra1, rb1, kbeg + 1);
+    if (kbeg < kend) {
+        la.template store<G::LDA_S>(As, ra0, tid);
+        lb.template store<G::LDB_S>(Bs, rb0, tid);
+    }
+    __syncthreads();
+
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NG = G::NG;
+    if (kbeg < kend) G::read_group(As, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
+
+    // Block kb sits in LDS stage s; the registers `cur` hold block kb+1 and
+    // `nxt` (free) receives block kb+2.
+    auto block = [&](int kb, int s, typename ALoader::VT *cur_a, typename BLoader::VT *cur_b,
+                     typename ALoader::VT *nxt_a, typename BLoader::VT *nxt_b) {
+        if (kb + 2 < kend) fetch(nxt_a, nxt_b, kb + 2);
+        const float *as = As + s * G::A_STAGE;
+        const float *bs = Bs + s * G::B_STAGE;
+#pragma unroll
+        for (int g = 0; g < NG - 1; ++g) {
+            G::read_group(as, bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of these MFMAs
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        if (kb + 1 < kend) {
+            la.template store<G::LDA_S>(As + (s ^ 1) * G::A_STAGE, cur_a, tid);
+            lb.template store<G::LDB_S>(Bs + (s ^ 1) * G::B_STAGE, cur_b, tid);
+        }
+        __syncthreads();
+        // unconditional, as in gemm_kernel (after the last block it reads a
+        // stage that is never used)
+        G::read_group(As + (s ^ 1) * G::A_STAGE, Bs + (s ^ 1) * G::B_STAGE, a_row, b_row, h, 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
+    };
+    // two blocks per trip so that each register set keeps one name
+    for (int kb = kbeg; kb < kend; kb += 2) {
+        block(kb, 0, ra1, rb1, ra0, rb0);
+        if (kb + 1 >= kend) break;
+        block(kb + 1, 1, ra0, rb0, ra1, rb1);
+    }
+
+    G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+}
+
 // The same contraction with ONE LDS stage: every K-block is loaded, stored
 // to LDS and multiplied in turn, with a barrier before the store (the last
 // block's reads are done) and one after it.  Nothing overlaps the global
