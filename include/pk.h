@@ -238,6 +238,8 @@ typedef struct {
                         evenly; convolution calls only (it needs the workspace) */
     int bres;        /* 1 = op(B) held whole in LDS while row tiles of A stream past; runs
                         only products with K == bk and N == bn (op(A) = A, op(B) = B) */
+    int kgroups;     /* groups of waves splitting K inside one work-group (1 = none); their
+                        partial tiles are added through LDS in group order */
 } pk_config_info;
 
 int pk_num_configs(void);

@@ -67,6 +67,15 @@ NN_SHORT_K_1S = [(64, 64, 64, 2, 2, 4, 4, 1), (128, 64, 64, 2, 2, 4, 4, 1), (128
 DEEP = [(64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 32, 2, 2, 4, 4, 1), (128, 64, 32, 2, 2, 4, 4, 1),
         (64, 128, 32, 2, 2, 4, 4, 1), (128, 128, 32, 2, 4, 4, 4, 2)]
 
+# K split among groups of waves inside the work-group ("_kN"): products with
+# few tiles and a long reduction (the paper's GEMM sweep).  (BM, BN, BK,
+# WAVES_M, WAVES_N, groups, steps loaded ahead (2: "_d2"), VA, VB, OCC)
+KSPLIT = [(64, 64, 16, 2, 2, 4, 1, 4, 4, 1), (64, 64, 32, 2, 2, 4, 1, 4, 4, 1), (64, 64, 32, 2, 2, 2, 1, 4, 4, 1),
+          (128, 64, 16, 2, 2, 4, 1, 4, 4, 1), (128, 128, 16, 2, 2, 2, 1, 4, 4, 1), (32, 64, 32, 1, 2, 4, 1, 4, 4, 1),
+          (32, 64, 16, 1, 2, 8, 1, 4, 4, 1),
+          (64, 64, 16, 2, 2, 4, 2, 4, 4, 1), (64, 64, 32, 2, 2, 4, 2, 4, 4, 1), (64, 64, 32, 2, 2, 2, 2, 4, 4, 1),
+          (32, 64, 32, 1, 2, 4, 2, 4, 4, 1), (32, 64, 16, 1, 2, 8, 2, 4, 4, 1)]
+
 # TT only needs a large, a small and a scalar-load tile.
 TT_TILES = [(128, 128, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 1, 1, 1)]
 
@@ -160,6 +169,12 @@ def main():
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
                            % (_name("gemm", t, layout), bm, bn, bk, wm, wn, ta, tb, va, vb, occ))
+        for t in (KSPLIT if layout != "tt" else []):
+            bm, bn, bk, wm, wn, ks, ahead, va, vb, occ = t
+            entries.append("PK_GEMM_KS(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
+                           % ("gemm_%dx%dx%d_w%dx%d_k%d_%s_v%d%d%s" % (bm, bn, bk, wm, wn, ks, layout, va, vb,
+                                                                    "_d2" if ahead == 2 else ""),
+                              bm, bn, bk, wm, wn, ks, ahead, ta, tb, va, vb, occ))
         for t in (DEEP if layout == "nn" else []):
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM_D(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"

@@ -154,7 +154,6 @@ const TunedShape kTuned[] = {
     {0, 1, 0, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_tn_v44_o2", 0},
     {0, 0, 1, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_nt_v44_o2", 0},
     {0, 0, 0, 2048, 2048, 2048, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
-    {0, 0, 0, 1024, 1024, 1024, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
     // VGG-16 block-first layers at batch 32 (3x3, stride 1)
     {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
     {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
@@ -167,6 +166,64 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},
     {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 6},
     {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 1},
+    // the other VGG-16 / ResNet-50 layers of the paper's tables at batch 1 and 4
+    // where the automated search (pk_tune_conv2d_fwd, whose candidates include
+    // the rules' own choice) found a faster configuration or split
+    {1, 0, 0, 12544, 128, 576, 3, 1, "conv_64x64x32_w2x2_v44_d2", 1},  // vgg16 conv2_1 b1 112x112x64->128 3x3 s1
+    {1, 0, 0, 12544, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_d2", 1},  // vgg16 conv2_2 b1 112x112x128->128 3x3 s1
+    {1, 0, 0, 3136, 256, 1152, 3, 1, "conv_64x64x32_w2x2_v44_d2", 2},  // vgg16 conv3_1 b1 56x56x128->256 3x3 s1
+    {1, 0, 0, 3136, 256, 2304, 3, 1, "conv_64x64x16_w2x2_v44", 6},  // vgg16 conv3_2 b1 56x56x256->256 3x3 s1
+    {1, 0, 0, 784, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_d2", 9},  // vgg16 conv4_1 b1 28x28x256->512 3x3 s1
+    {1, 0, 0, 784, 512, 4608, 3, 1, "conv_128x128x64_w2x4_v44_o2", 9},  // vgg16 conv4_2 b1 28x28x512->512 3x3 s1
+    {1, 0, 0, 196, 512, 4608, 3, 1, "conv_64x64x64_w2x2_v44", 8},  // vgg16 conv5_1 b1 14x14x512->512 3x3 s1
+    {1, 0, 0, 3136, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b1 56x56x64->256 1x1 s1
+    {1, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
+    {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x64_w2x2_v44", 8},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
+    {1, 0, 0, 3136, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_d2", 6},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
+    {1, 0, 0, 784, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44", 8},  // resnet50 conv2_5 b1 56x56x64->64 3x3 s2
+    {1, 0, 0, 784, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b1 28x28x64->256 1x1 s1
+    {1, 0, 0, 784, 512, 256, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
+    {1, 0, 0, 784, 128, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 6},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
+    {1, 0, 0, 784, 128, 1152, 3, 1, "conv_64x64x16_w2x2_v44", 9},  // resnet50 conv3_4 b1 28x28x128->128 3x3 s1
+    {1, 0, 0, 784, 512, 128, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 1},  // resnet50 conv3_5 b1 28x28x128->512 1x1 s1
+    {1, 0, 0, 784, 128, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 6},  // resnet50 conv3_6 b1 28x28x512->128 1x1 s1
+    {1, 0, 0, 196, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44", 16},  // resnet50 conv3_7 b1 28x28x128->128 3x3 s2
+    {1, 0, 0, 196, 512, 128, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 1},  // resnet50 conv4_1 b1 14x14x128->512 1x1 s1
+    {1, 0, 0, 196, 1024, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 6},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
+    {1, 0, 0, 196, 256, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 8},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
+    {1, 0, 0, 196, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44", 12},  // resnet50 conv4_4 b1 14x14x256->256 3x3 s1
+    {1, 0, 0, 196, 1024, 256, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 8},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
+    {1, 0, 0, 196, 256, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 12},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
+    {1, 0, 0, 49, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44", 16},  // resnet50 conv4_7 b1 14x14x256->256 3x3 s2
+    {1, 0, 0, 49, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 4},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
+    {1, 0, 0, 49, 2048, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 12},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
+    {1, 0, 0, 49, 512, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 12},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
+    {1, 0, 0, 49, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44", 16},  // resnet50 conv5_4 b1 7x7x512->512 3x3 s1
+    {1, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
+    {1, 0, 0, 49, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 16},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
+    {1, 0, 0, 50176, 128, 1152, 3, 1, "conv_128x128x16_w2x4_v44_o2_p", 3},  // vgg16 conv2_2 b4 112x112x128->128 3x3 s1
+    {1, 0, 0, 12544, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_d2", 1},  // vgg16 conv3_1 b4 56x56x128->256 3x3 s1
+    {1, 0, 0, 12544, 256, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2", 6},  // vgg16 conv3_2 b4 56x56x256->256 3x3 s1
+    {1, 0, 0, 3136, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44_d2", 3},  // vgg16 conv4_1 b4 28x28x256->512 3x3 s1
+    {1, 0, 0, 3136, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2", 11},  // vgg16 conv4_2 b4 28x28x512->512 3x3 s1
+    {1, 0, 0, 50176, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b4 230x230x3->64 7x7 s2
+    {1, 0, 0, 12544, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b4 56x56x64->256 1x1 s1
+    {1, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
+    {1, 0, 0, 12544, 64, 576, 3, 1, "conv_64x64x64_w2x2_v44", 1},  // resnet50 conv2_3 b4 56x56x64->64 3x3 s1
+    {1, 0, 0, 3136, 64, 576, 3, 2, "conv_64x64x64_w2x2_v44", 8},  // resnet50 conv2_5 b4 56x56x64->64 3x3 s2
+    {1, 0, 0, 3136, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_d2", 1},  // resnet50 conv3_2 b4 28x28x256->512 1x1 s1
+    {1, 0, 0, 3136, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44", 4},  // resnet50 conv3_4 b4 28x28x128->128 3x3 s1
+    {1, 0, 0, 3136, 512, 128, 1, 1, "gemm_64x64x32_w2x2_nn_v44_d2", 1},  // resnet50 conv3_5 b4 28x28x128->512 1x1 s1
+    {1, 0, 0, 3136, 128, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 2},  // resnet50 conv3_6 b4 28x28x512->128 1x1 s1
+    {1, 0, 0, 784, 128, 1152, 3, 2, "conv_64x64x16_w2x2_v44", 9},  // resnet50 conv3_7 b4 28x28x128->128 3x3 s2
+    {1, 0, 0, 784, 256, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 4},  // resnet50 conv4_3 b4 14x14x512->256 1x1 s1
+    {1, 0, 0, 784, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_d2", 9},  // resnet50 conv4_4 b4 14x14x256->256 3x3 s1
+    {1, 0, 0, 784, 256, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 4},  // resnet50 conv4_6 b4 14x14x1024->256 1x1 s1
+    {1, 0, 0, 196, 256, 2304, 3, 2, "conv_64x64x64_w2x2_v44", 16},  // resnet50 conv4_7 b4 14x14x256->256 3x3 s2
+    {1, 0, 0, 196, 2048, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 4},  // resnet50 conv5_2 b4 7x7x1024->2048 1x1 s1
+    {1, 0, 0, 196, 512, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 8},  // resnet50 conv5_3 b4 7x7x1024->512 1x1 s1
+    {1, 0, 0, 196, 2048, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 6},  // resnet50 conv5_5 b4 7x7x512->2048 1x1 s1
+    {1, 0, 0, 196, 512, 2048, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 8},  // resnet50 conv5_6 b4 7x7x2048->512 1x1 s1
 };
 
 // Entries recorded at run time by pk_tune_sgemm / pk_tune_conv2d_fwd; they
@@ -217,14 +274,31 @@ bool record_tuned(const TunedShape &t)
     return true;
 }
 
+// A B-resident configuration runs only products whose K is its one K-block
+// and whose N is a multiple of its column block.
+// (Its C stores address a tile's rows in 32 bits: (BM + 1) rows of ldc floats.)
+bool bres_fits(const Config *c, int64_t N, int64_t K, int64_t ldc)
+{
+    return !c->bres || (N % c->bn == 0 && K == c->bk &&
+                        (int64_t)(c->bm + 1) * ldc * (int64_t)sizeof(float) < ((int64_t)1 << 31));
+}
+
 // Shapes outside the table, from the same measurements:
 //   - products with at least 4 work-groups of 128 x 128 per CU and K >= 512:
 //     256 x 256 tiles on 8 waves (128 x 64 per wave, 2 waves per SIMD): the
 //     fewest LDS reads and the least L2 traffic per MFMA;
-//   - everything smaller: 64 x 64 tiles, which keep 4+ waves per SIMD busy;
-//     K-blocks of 32, or 16 when K itself is that short;
+//   - K <= 64: 64 x 64 tiles; for NN products with K == 64 and N a multiple
+//     of 64, the B-resident form (the whole reduction is one K-block);
+//   - longer reductions with at most one 32 x 64 tile per CU: the reduction
+//     split among 4 groups of 2 waves inside the work-group, loads two steps
+//     ahead (a lone work-group per CU walks a quarter of the K-blocks);
+//     with at most one 64 x 64 tile per CU, 2 groups of 4 waves on 64 x 64
+//     tiles (the 64 .. 1024 sweep of M, N, K at K >= 128: 1.3-1.8x over
+//     one group, every shape);
+//   - everything larger: 64 x 64 tiles, which keep 4+ waves per SIMD busy;
+//     K-blocks of 32;
 //   - unaligned operands: 4-byte loads.
-const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, bool vec_ok)
+const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t ldc, bool vec_ok)
 {
     static const char *layout[2][2] = {{"nn", "nt"}, {"tn", "tt"}};
     const char *lay = layout[ta][tb];
@@ -236,19 +310,19 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, bool 
         snprintf(name, sizeof(name), big ? "gemm_128x128x16_w2x2_%s_v44" : "gemm_64x64x16_w2x2_%s_v44", lay);
     } else if (ceil_div(M, 128) * ceil_div(N, 128) >= 4 * kCUs && K >= 512) {
         snprintf(name, sizeof(name), "gemm_256x256x32_w2x4_%s_v44_o2", lay);
+    } else if (K <= 64) {
+        snprintf(name, sizeof(name), "gemm_64x64x64_w2x2_%s_v44_br", lay);
+        const Config *c = !ta && !tb ? find_config(name) : nullptr;
+        if (c && bres_fits(c, N, K, ldc)) return c;
+        snprintf(name, sizeof(name), "gemm_64x64x16_w2x2_%s_v44", lay);
+    } else if (ceil_div(M, 32) * ceil_div(N, 64) <= kCUs) {
+        snprintf(name, sizeof(name), "gemm_32x64x32_w1x2_k4_%s_v44_d2", lay);
+    } else if (ceil_div(M, 64) * ceil_div(N, 64) <= kCUs) {
+        snprintf(name, sizeof(name), "gemm_64x64x32_w2x2_k2_%s_v44_d2", lay);
     } else {
-        snprintf(name, sizeof(name), K <= 64 ? "gemm_64x64x16_w2x2_%s_v44" : "gemm_64x64x32_w2x2_%s_v44", lay);
+        snprintf(name, sizeof(name), "gemm_64x64x32_w2x2_%s_v44", lay);
     }
     return find_config(name);
-}
-
-// A B-resident configuration runs only products whose K is its one K-block
-// and whose N is a multiple of its column block.
-// (Its C stores address a tile's rows in 32 bits: (BM + 1) rows of ldc floats.)
-bool bres_fits(const Config *c, int64_t N, int64_t K, int64_t ldc)
-{
-    return !c->bres || (N % c->bn == 0 && K == c->bk &&
-                        (int64_t)(c->bm + 1) * ldc * (int64_t)sizeof(float) < ((int64_t)1 << 31));
 }
 
 bool conv_config_fits(const Config *c, bool va4, bool vb4)
@@ -283,7 +357,9 @@ const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4)
 // 14x14x512 layer at batch 32.
 int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 {
-    if (c->bres) return 1;  // its one K-block is the whole reduction
+    // a B-resident form's one K-block is the whole reduction; a K-split form
+    // splits K inside the work-group
+    if (c->bres || c->kgroups > 1) return 1;
     const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
     const int64_t nkb = ceil_div(K, c->bk);
     if (tiles >= 4 * kCUs) return 1;
@@ -428,7 +504,7 @@ int pk_get_config(int idx, pk_config_info *info)
     info->bk = c->bk;
     info->waves_m = c->waves_m;
     info->waves_n = c->waves_n;
-    info->threads = 64 * c->waves_m * c->waves_n;
+    info->threads = 64 * c->waves_m * c->waves_n * c->kgroups;
     info->trans_a = c->trans_a;
     info->trans_b = c->trans_b;
     info->vec_a = c->vec_a;
@@ -439,6 +515,7 @@ int pk_get_config(int idx, pk_config_info *info)
     info->persistent = c->persistent;
     info->streamk = c->streamk;
     info->bres = c->bres;
+    info->kgroups = c->kgroups;
     return PK_OK;
 }
 
@@ -542,7 +619,7 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float al
         const TunedShape *t = find_tuned(0, ta, tb, M, N, K, 0, 0, &tbuf) ? &tbuf : nullptr;
         c = t ? find_config(t->config) : nullptr;
         if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K, ldc))) c = nullptr;
-        if (!c) c = select_gemm(ta, tb, M, N, K, vec_ok);
+        if (!c) c = select_gemm(ta, tb, M, N, K, ldc, vec_ok);
         if (!c) return PK_ERR_NOT_SUPPORTED;
     }
     KernelArgs a;
@@ -587,7 +664,7 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
         const bool direct_ok = !gemm_path && pk::direct_conv_fits(nullptr, W, Wo, Cout, KH, KW, Cin, sh, sw) && N <= 65535;
         if (direct_ok && !(tuned && v4)) return 0;
         c = (tuned && v4) ? find_config(tuned->config) : nullptr;
-        if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
+        if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cout, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
     }
     if (!c || c->kind == pk::KIND_DIRECT) return 0;
     if (c->streamk) {
@@ -677,7 +754,10 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         } else {
             c = (tuned && vec_ok) ? find_config(tuned->config) : nullptr;
             if (c && !bres_fits(c, Cout, Cin, Cout)) c = nullptr;
-            if (!c) c = select_gemm(0, 0, M, Cout, Cin, vec_ok);
+            if (!c) c = select_gemm(0, 0, M, Cout, Cin, Cout, vec_ok);
+            // a forced split needs a form that splits K across work-groups
+            if (c && t_forced_splits > 1 && (c->bres || c->kgroups > 1))
+                c = find_config(vec_ok ? "gemm_64x64x32_w2x2_nn_v44" : "gemm_64x64x16_w2x2_nn_v11");
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     } else {
@@ -729,7 +809,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         } else if (was_forced) {
             return planned ? PK_ERR_WORKSPACE : PK_ERR_NOT_SUPPORTED;
         } else {
-            c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, vec_ok) : select_conv(M, Cout, va4, vb4);
+            c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cout, vec_ok) : select_conv(M, Cout, va4, vb4);
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     }
@@ -759,7 +839,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     const size_t per_split = (size_t)M * (size_t)Cout * sizeof(float);
     if (t_forced_splits > 0) {
         splits = t_forced_splits;
-        if (splits > 1 && c->bres) return PK_ERR_NOT_SUPPORTED;
+        if (splits > 1 && (c->bres || c->kgroups > 1)) return PK_ERR_NOT_SUPPORTED;
         if (splits > 1 && (!workspace || workspace_bytes < (size_t)splits * per_split)) return PK_ERR_WORKSPACE;
     } else {
         const bool tuned_cfg = tuned && strcmp(c->name, tuned->config) == 0 && tuned->splits > 0;
@@ -1093,7 +1173,9 @@ int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t 
     hipStream_t s = (hipStream_t)stream;
     EventPair ev;
     if (!ev.ok) return PK_ERR_LAUNCH;
-    static const int kSplits[] = {1, 2, 3, 4, 6, 8};
+    // the splits tried: a fixed ladder plus each configuration's own rule
+    // split (so the choice the rules would make is always among the candidates)
+    static const int kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16};
     const Config *best = nullptr;
     int best_splits = 1;
     float best_ms = 0.f;
@@ -1107,10 +1189,17 @@ int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t 
             const bool takes = gemm_path ? (c->kind == pk::KIND_GEMM && !c->trans_a && !c->trans_b && !c->single_stage)
                                          : (c->kind == pk::KIND_CONV || c->kind == pk::KIND_DIRECT);
             if (!takes) continue;
-            for (int sp : kSplits) {
-                if (sp > 1 && (c->kind == pk::KIND_DIRECT || c->streamk ||
-                               workspace_bytes < (size_t)sp * M * Cout * sizeof(float)))
-                    break;
+            int ladder[sizeof(kSplits) / sizeof(kSplits[0]) + 1];
+            int nl = 0;
+            for (int sp : kSplits) ladder[nl++] = sp;
+            const int rule = choose_splits(c, M, Cout, K);
+            bool listed = false;
+            for (int j = 0; j < nl; ++j) listed = listed || ladder[j] == rule;
+            if (!listed) ladder[nl++] = rule;
+            for (int j = 0; j < nl; ++j) {
+                const int sp = ladder[j];
+                if (sp > 1 && (c->kind == pk::KIND_DIRECT || c->streamk || c->bres || c->kgroups > 1)) break;
+                if (sp > 1 && workspace_bytes < (size_t)sp * M * Cout * sizeof(float)) continue;
                 scope.force(c, sp);
                 const float ms = time_calls(call, iters, s, ev, &st);
                 if (st == PK_ERR_LAUNCH) return st;

@@ -34,7 +34,8 @@ struct Config {
     // work-groups of this instance one CU holds at once (occupancy query;
     // beta != 0 selects the epilogue that reads C).  Set for stream-K instances.
     int (*resident)(int beta);
-    int bres;  // 1 = op(B) resident in LDS: runs only products with K == bk and N == bn
+    int bres;  // 1 = op(B) resident in LDS: runs only products with K == bk and N a multiple of bn
+    int kgroups = 1;  // groups of waves splitting K inside the work-group (gemm_ksplit_kernel)
 };
 
 // The registry (defined with the kernel instances, host side only).

@@ -128,6 +128,26 @@ static hipError_t launch_gemm_bres(const KernelArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
+// K split among KS groups of waves inside each work-group (one work-group per
+// tile, no split across work-groups).
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int KS, int AHEAD, int AMODE, bool B_KCONTIG, int VA,
+          int VB, int OCC>
+static hipError_t launch_gemm_ksplit(const KernelArgs &a, hipStream_t stream)
+{
+    if (a.splits > 1) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), 1);
+    const dim3 block(64 * WAVES_M * WAVES_N * KS);
+    if (reads_c<AMODE>(a)) {
+        hipLaunchKernelGGL(
+            (gemm_ksplit_kernel<BM, BN, BK, WAVES_M, WAVES_N, KS, AHEAD, AMODE, B_KCONTIG, VA, VB, OCC, true>), grid, block,
+            0, stream, a);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((gemm_ksplit_kernel<BM, BN, BK, WAVES_M, WAVES_N, KS, AHEAD, AMODE, B_KCONTIG, VA, VB, OCC, false>),
+                       grid, block, 0, stream, a);
+    return hipGetLastError();
+}
+
 // Loads two K-blocks ahead (same grid as launch_gemm).
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
 static hipError_t launch_gemm_deep(const KernelArgs &a, hipStream_t stream)
@@ -194,6 +214,12 @@ static constexpr int lds_bytes()
     {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC, 0,                                    \
      lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),                \
      &launch_gemm_deep<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>}
+
+#define PK_GEMM_KS(name, BM, BN, BK, WM, WN, KS, AHEAD, TA, TB, VA, VB, OCC)                         \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, VA, VB, OCC, 0,                                    \
+     KS * lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),           \
+     &launch_gemm_ksplit<BM, BN, BK, WM, WN, KS, AHEAD, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>, \
+     0, 0, nullptr, 0, KS}
 
 #define PK_CONV_D(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                               \
     {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 0,                                      \

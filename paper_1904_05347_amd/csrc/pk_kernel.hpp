@@ -139,10 +139,17 @@ struct KContigLoader {
         for (int i = 0; i < LOADS; ++i)
             v[i] = (row_ok[i] && k_ok) ? Vec<VEC>::load(ptr[i]) : Vec<VEC>::zero();
     }
+    // the thread's offsets were fixed by init
+    __device__ __forceinline__ void load(VT *v, int k0, int K, int) const { load(v, k0, K); }
     __device__ __forceinline__ void advance()
     {
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) ptr[i] += BK;
+    }
+    __device__ __forceinline__ void advance_by(int blocks)
+    {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) ptr[i] += (int64_t)BK * blocks;
     }
     // LDS tile [ROWS][BK + PAD]
     template <int LD>
@@ -179,9 +186,9 @@ struct MContigLoader {
         }
         ptr = base + (int64_t)kbeg * BK * ld + col0;
     }
-    __device__ __forceinline__ void load(VT *v, int k0, int K) const
+    // tid is the thread's index within the NT threads that share the panel
+    __device__ __forceinline__ void load(VT *v, int k0, int K, int tid) const
     {
-        const int tid = threadIdx.x;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
             const int c = (tid + i * NT) % CPR * VEC;
@@ -190,7 +197,9 @@ struct MContigLoader {
             v[i] = ok ? Vec<VEC>::load(ptr + (int64_t)r * ld + c) : Vec<VEC>::zero();
         }
     }
+    __device__ __forceinline__ void load(VT *v, int k0, int K) const { load(v, k0, K, (int)threadIdx.x); }
     __device__ __forceinline__ void advance() { ptr += (int64_t)BK * ld; }
+    __device__ __forceinline__ void advance_by(int blocks) { ptr += (int64_t)BK * ld * blocks; }
     // LDS tile [BK][COLS + PAD]
     template <int LD>
     __device__ __forceinline__ void store(float *lds, const VT *v, int tid) const
@@ -667,6 +676,155 @@ gemm_deep_kernel(KernelArgs p)
     }
 
     G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+}
+
+// The same contraction with the K dimension split INSIDE the work-group,
+// for products with few C tiles and a long reduction (the paper's GEMM sweep:
+// M, N <= 1024 with K up to 1024 gives 1-256 tiles of 64 x 64, so one
+// work-group per tile walks 16-32 K-blocks one after the other, each paying
+// the global-load latency).  The work-group holds KS groups of
+// WAVES_M x WAVES_N waves; group g multiplies the K-blocks g, g + KS,
+// g + 2 KS, ... of the tile through its own two LDS stages (the blocked
+// identity over a partition of K, Section 3.1.1), so the chain of dependent
+// K-blocks is KS times shorter and KS times more waves work on each tile.
+// At the end the groups' partial tiles are added through LDS in group order
+// (deterministic; no workspace, no atomics) and group 0 writes C.  Every
+// group runs the same number of K-block steps (a group past the last block
+// loads zeros), so the work-group's barriers line up.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int KS, int AHEAD, int AMODE, bool B_KCONTIG, int VA, int VB,
+          int OCC, bool BETA>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N * KS) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_ksplit_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, AMODE, B_KCONTIG, VA, VB> G;
+    typedef typename G::ALoader ALoader;
+    typedef typename G::BLoader BLoader;
+    static_assert(AMODE != A_CONV, "dense operands only");
+    static_assert(AHEAD == 1 || AHEAD == 2, "loads one or two steps ahead");
+    constexpr int GT = G::NT;                      // threads per group
+    constexpr int ACCF = G::RM * G::RN * 16;       // accumulator floats per lane
+    static_assert((KS - 1) * GT * ACCF <= KS * G::LDS_FLOATS, "partial tiles fit in the stages");
+
+    __shared__ __attribute__((aligned(16))) float smem[KS * G::LDS_FLOATS];
+
+    const int grp = threadIdx.x / GT;
+    const int tid = threadIdx.x - grp * GT;
+    float *As = smem + grp * G::LDS_FLOATS;        // [2][A_STAGE] of this group
+    float *Bs = As + 2 * G::A_STAGE;               // [2][B_STAGE]
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+
+    if (p.nbatch > 1) {  // product blockIdx.y of a batch
+        const int64_t bz = blockIdx.y;
+        p.A += bz * p.stride_a;
+        p.B += bz * p.stride_b;
+        p.C += bz * p.stride_c;
+    }
+    int tm, tn;
+    tile_coords(p, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int nkb = (p.K + BK - 1) / BK;
+    const int steps = (nkb + KS - 1) / KS;  // K-block steps of every group
+
+    ALoader la;
+    BLoader lb;
+    la.init(p.A, p.lda, m0, p.M, grp, tid);
+    lb.init(p.B, p.ldb, n0, p.N, grp, tid);
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename ALoader::VT ra0[ALoader::LOADS], ra1[AHEAD == 2 ? ALoader::LOADS : 1];
+    typename BLoader::VT rb0[BLoader::LOADS], rb1[AHEAD == 2 ? BLoader::LOADS : 1];
+
+    // step st of group g multiplies K-block st*KS + g (zeros past the end:
+    // the loaders read nothing at k >= K); steps are fetched in order
+    auto fetch = [&](typename ALoader::VT *ra, typename BLoader::VT *rb, int st) {
+        const int k0 = (st * KS + grp) * BK;
+        la.load(ra, k0, p.K, tid);
+        lb.load(rb, k0, p.K, tid);
+        la.advance_by(KS);
+        lb.advance_by(KS);
+    };
+    fetch(ra0, rb0, 0);
+    if constexpr (AHEAD == 2) {
+        if (1 < steps) fetch(ra1, rb1, 1);
+    }
+    la.template store<G::LDA_S>(As, ra0, tid);
+    lb.template store<G::LDB_S>(Bs, rb0, tid);
+    __syncthreads();
+
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NG = G::NG;
+    G::read_group(As, Bs, a_row, b_row, h, 0, fa[0], fb[0]);
+
+    // Step st sits in LDS stage s.  With AHEAD = 1 the registers `nxt`
+    // receive step st+1 and are stored at the end of this step; with
+    // AHEAD = 2 `cur` already holds step st+1 (stored at the end of this
+    // step) and `nxt` receives step st+2.  Every condition is the same in
+    // all groups, so the work-group's barriers line up.
+    auto step = [&](int st, int s, typename ALoader::VT *cur_a, typename BLoader::VT *cur_b,
+                    typename ALoader::VT *nxt_a, typename BLoader::VT *nxt_b) {
+        if (st + AHEAD < steps) fetch(nxt_a, nxt_b, st + AHEAD);
+        const float *as = As + s * G::A_STAGE;
+        const float *bs = Bs + s * G::B_STAGE;
+#pragma unroll
+        for (int g = 0; g < NG - 1; ++g) {
+            G::read_group(as, bs, a_row, b_row, h, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        if (st + 1 < steps) {
+            la.template store<G::LDA_S>(As + (s ^ 1) * G::A_STAGE, cur_a, tid);
+            lb.template store<G::LDB_S>(Bs + (s ^ 1) * G::B_STAGE, cur_b, tid);
+        }
+        __syncthreads();
+        G::read_group(As + (s ^ 1) * G::A_STAGE, Bs + (s ^ 1) * G::B_STAGE, a_row, b_row, h, 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
+    };
+    if constexpr (AHEAD == 1) {
+        for (int st = 0, s = 0; st < steps; ++st, s ^= 1) step(st, s, ra0, rb0, ra0, rb0);
+    } else {
+        // two steps per trip so that each register set keeps one name
+        for (int st = 0; st < steps; st += 2) {
+            step(st, 0, ra1, rb1, ra0, rb0);
+            if (st + 1 >= steps) break;
+            step(st + 1, 1, ra0, rb0, ra1, rb1);
+        }
+    }
+
+    // groups 1..KS-1 leave their partial tiles in LDS, group 0 adds them in
+    // group order.  Every stage read that feeds an MFMA is behind the last
+    // barrier; the one read after it (group 0 of the next stage, into fa[0])
+    // is never used, since NG is even and the last mma_group takes fa[1].
+    if (grp > 0) {
+        float *slot = smem + (grp - 1) * GT * ACCF + tid;
+#pragma unroll
+        for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+            for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) slot[((i * G::RN + j) * 16 + r) * GT] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+        for (int q = 1; q < KS; ++q) {
+            const float *slot = smem + (q - 1) * GT * ACCF + tid;
+#pragma unroll
+            for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[i][j][r] += slot[((i * G::RN + j) * 16 + r) * GT];
+        }
+        G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, 0);
+    }
 }
 
 // The same contraction with ONE LDS stage: every K-block is loaded, stored

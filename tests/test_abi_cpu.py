@@ -180,7 +180,8 @@ def test_config_space(pk):
     names = [c["name"] for c in cfgs]
     assert len(set(names)) == len(names)
     for c in cfgs:
-        assert c["threads"] == 64 * c["waves_m"] * c["waves_n"]
+        assert c["threads"] == 64 * c["waves_m"] * c["waves_n"] * c["kgroups"]
+        assert c["kgroups"] == 1 or (c["kind"] == 0 and not c["persistent"] and not c["streamk"])
         assert c["lds_bytes"] <= 160 * 1024
         if c["kind"] == 2:  # tiled direct convolution: one LDS input patch
             continue
@@ -195,7 +196,10 @@ def test_config_space(pk):
         if c["bres"]:  # two stages of A, and B held whole (n-major)
             assert c["lds_bytes"] == 4 * (2 * a_tile + c["bn"] * (c["bk"] + 4)), c["name"]
             continue
-        assert c["lds_bytes"] == c["stages"] * 4 * (a_tile + b_tile), c["name"]
+        # K split inside the work-group: every group of waves has its own stages
+        assert c["kgroups"] >= 1
+        assert c["threads"] == 64 * c["waves_m"] * c["waves_n"] * c["kgroups"] <= 1024, c["name"]
+        assert c["lds_bytes"] == c["kgroups"] * c["stages"] * 4 * (a_tile + b_tile), c["name"]
         assert c["lds_bytes"] <= 160 * 1024
     # every GEMM layout has a 16-byte and a scalar-load instance
     for ta in (0, 1):

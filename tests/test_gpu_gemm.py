@@ -164,6 +164,41 @@ def test_every_gemm_config_forced():
             assert np.array_equal(out.astype(np.float64), ref), (cfg["name"], M, N, K)
 
 
+def test_ksplit_configs():
+    """K split among groups of waves inside the work-group: a long reduction
+    that does not divide into the groups' K-blocks (groups past the end add
+    zeros), ragged tiles, every layout; integer data, so the partial tiles
+    added in group order must equal the oracle bit for bit; with beta = 0 and
+    C prefilled with NaN every output must be written."""
+    torch, pk = require_gpu()
+    ran = 0
+    for cfg in pk.configs():
+        if cfg["kind"] != 0 or cfg["kgroups"] == 1:
+            continue
+        ta = "T" if cfg["trans_a"] else "N"
+        tb = "T" if cfg["trans_b"] else "N"
+        # multiples of 4 (the 4-wide loads), ragged against tiles and K-blocks
+        for M, N, K, beta in [(132, 68, 1000, 0.5), (64, 64, 1024, 0.0), (36, 200, 92, 0.0)]:
+            rng = np.random.default_rng(M * 7 + N + K)
+            A = wl.integers(rng, M * K).reshape((K, M) if ta == "T" else (M, K))
+            B = wl.integers(rng, K * N).reshape((N, K) if tb == "T" else (K, N))
+            C = wl.integers(rng, M * N).reshape(M, N) if beta else np.full((M, N), np.nan, np.float32)
+            dA, dB, dC = dev(A), dev(B), dev(C)
+            pk.force_config(cfg["name"])
+            try:
+                st = pk.binding.sgemm(ta, tb, M, N, K, 1.0, dA.data_ptr(), A.shape[1], dB.data_ptr(), B.shape[1],
+                                      beta, dC.data_ptr(), N)
+                used = pk.last_config_name()
+            finally:
+                pk.force_config(None)
+            assert st == 0 and used == cfg["name"]
+            ref, _ = oracle.sgemm(ta, tb, M, N, K, 1.0, A, A.shape[1], B, B.shape[1], beta,
+                                  C if beta else np.zeros((M, N), np.float32), N)
+            assert np.array_equal(host(dC).astype(np.float64), ref), (cfg["name"], M, N, K)
+            ran += 1
+    assert ran >= 36
+
+
 def test_column_major_swap_identity():
     """A column-major C = A B is the row-major call with operands swapped."""
     torch, pk = require_gpu()
