@@ -74,6 +74,37 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K,
              float beta, float *C, int64_t ldc, void *stream);
 
 /*
+ * Bytes of device workspace that lets pk_sgemm_ws split the reduction K of
+ * this product across work-groups, for the configuration the next
+ * pk_sgemm_ws call on this thread would choose with 16-byte aligned, tightly
+ * packed operands (a forced one included); 0 when that configuration needs
+ * none.  A split keeps one M x N partial sum per slice of K; a stream-K
+ * configuration two partial tiles per resident work-group and one arrival
+ * counter per tile of C.  Products whose tiles fill the CUs take no split.
+ * Host-only apart from an occupancy query of the kernel.
+ */
+size_t pk_sgemm_workspace_bytes(char transA, char transB, int64_t M, int64_t N, int64_t K);
+
+/*
+ * pk_sgemm with a workspace (the same operation, arguments, quick returns
+ * and determinism; error positions as there, then 14 = workspace).
+ *   workspace    optional device buffer of workspace_bytes; with at least
+ *                pk_sgemm_workspace_bytes() a product with few tiles of C
+ *                and a long K may split K across work-groups (the partial
+ *                products, each alpha-scaled, are added in slice order by a
+ *                second kernel that also applies beta * C) or run stream-K
+ *                (16-byte alignment needed).  NULL / too small selects a
+ *                configuration and split that need none.  It must not
+ *                overlap A, B or C.  Contents on return are unspecified.
+ *                Two calls that overlap in time must not share a workspace.
+ */
+int pk_sgemm_ws(char transA, char transB, int64_t M, int64_t N, int64_t K,
+                float alpha, const float *A, int64_t lda,
+                const float *B, int64_t ldb,
+                float beta, float *C, int64_t ldc,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Output size of a convolution window (the stride S and window W columns of
  * the paper's layer tables): Ho = floor((H + pt + pb - KH) / sh) + 1, and the
  * same for Wo.  Pads >= 0, strides >= 1, window >= 1 and not larger than the
@@ -170,8 +201,9 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
  * configuration that the paper makes by hand for each of its devices
  * (Section 5) and plans to automate (Section 7).  Every compiled
  * configuration that takes the problem (the single-LDS-stage ablation forms
- * excepted) -- and for the convolution every split of the reduction from 1
- * to 8 that the workspace allows -- runs one untimed call and then three
+ * excepted) -- with each split of the reduction in {1, 2, 3, 4, 6, 8, 12,
+ * 16} and the configuration's own rule split that the workspace holds (none
+ * for stream-K, B-resident and direct forms) -- runs one untimed call and then three
  * timed runs of `iters` calls (more for short calls: up to about 1 ms per
  * run) on the caller's operands, on `stream` (HIP events; the median run
  * counts); the fastest is recorded in a process-wide
@@ -182,7 +214,7 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
  *   sh == sw only (else PK_ERR_NOT_SUPPORTED after validation).
  * The call synchronizes the stream.  C (y) is written many times: with
  * beta != 0 its final contents are unspecified, so pass a scratch C.
- * Arguments and error positions are those of pk_sgemm / pk_conv2d_fwd, then
+ * Arguments and error positions are those of pk_sgemm_ws / pk_conv2d_fwd, then
  * iters (>= 1), stream, result (non-NULL).  An empty problem records
  * nothing (result->config is "").  The table holds 256 entries (else
  * PK_ERR_NOT_SUPPORTED); pk_tune_reset() empties it.
@@ -196,8 +228,9 @@ typedef struct {
 
 int pk_tune_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K,
                   float alpha, const float *A, int64_t lda, const float *B, int64_t ldb,
-                  float beta, float *C, int64_t ldc, int iters, void *stream,
-                  pk_tune_result *result);
+                  float beta, float *C, int64_t ldc,
+                  void *workspace, size_t workspace_bytes,
+                  int iters, void *stream, pk_tune_result *result);
 int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
                        const float *f, int64_t KH, int64_t KW, int64_t Cout,
                        int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb, int64_t pr,

@@ -59,6 +59,9 @@ class TuneResult(ctypes.Structure):
 SIGNATURES = {
     "pk_sgemm": (ctypes.c_int, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64, ctypes.c_float, _p, _i64,
                                 _p, _i64, ctypes.c_float, _p, _i64, _p]),
+    "pk_sgemm_workspace_bytes": (ctypes.c_size_t, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64]),
+    "pk_sgemm_ws": (ctypes.c_int, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64, ctypes.c_float, _p, _i64,
+                                   _p, _i64, ctypes.c_float, _p, _i64, _p, ctypes.c_size_t, _p]),
     "pk_conv2d_out_dims": (ctypes.c_int, [_i64] * 10 + [_p, _p]),
     "pk_conv2d_same_pads": (ctypes.c_int, [_i64] * 6 + [_p]),
     "pk_conv2d_workspace_bytes": (ctypes.c_size_t, [_i64] * 13),
@@ -70,7 +73,7 @@ SIGNATURES = {
                                               _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
                                               _p, ctypes.c_size_t, _p]),
     "pk_tune_sgemm": (ctypes.c_int, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64, ctypes.c_float, _p, _i64,
-                                     _p, _i64, ctypes.c_float, _p, _i64, ctypes.c_int, _p,
+                                     _p, _i64, ctypes.c_float, _p, _i64, _p, ctypes.c_size_t, ctypes.c_int, _p,
                                      ctypes.POINTER(TuneResult)]),
     "pk_tune_conv2d_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
                                           _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
@@ -126,6 +129,17 @@ def sgemm(trans_a, trans_b, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream
     """pk_sgemm on raw device addresses; returns the status code."""
     return load().pk_sgemm(_trans(trans_a), _trans(trans_b), M, N, K, alpha, A, lda, B, ldb,
                            beta, C, ldc, stream)
+
+
+def sgemm_ws(trans_a, trans_b, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, workspace=None,
+             workspace_bytes=0, stream=None) -> int:
+    """pk_sgemm_ws on raw device addresses; returns the status code."""
+    return load().pk_sgemm_ws(_trans(trans_a), _trans(trans_b), M, N, K, alpha, A, lda, B, ldb,
+                              beta, C, ldc, workspace, workspace_bytes, stream)
+
+
+def sgemm_workspace_bytes(trans_a, trans_b, M, N, K) -> int:
+    return load().pk_sgemm_workspace_bytes(_trans(trans_a), _trans(trans_b), M, N, K)
 
 
 def conv2d_fwd_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo,
@@ -262,12 +276,15 @@ def _ld_2d(t, what):
     return max(t.stride(0), t.size(1), 1)
 
 
-def gemm(a, b, c=None, alpha=1.0, beta=0.0, trans_a=False, trans_b=False):
+def gemm(a, b, c=None, alpha=1.0, beta=0.0, trans_a=False, trans_b=False, workspace=None):
     """C = alpha * op(a) @ op(b) + beta * c on the current stream.
 
     ``a`` is stored M x K (or K x M with trans_a), ``b`` K x N (or N x K with
     trans_b); both are row-major views with unit column stride.  Returns c
-    (allocated when None; then beta must be 0).
+    (allocated when None; then beta must be 0).  workspace (a float32 device
+    tensor) lets a product with few tiles split K across work-groups (see
+    ``sgemm_workspace_bytes``); when None, one of the size the library asks
+    for is allocated.
     """
     import torch
     _check_f32_cuda(a, "a")
@@ -285,9 +302,17 @@ def gemm(a, b, c=None, alpha=1.0, beta=0.0, trans_a=False, trans_b=False):
     if tuple(c.shape) != (M, N):
         raise ValueError("c must be %d x %d" % (M, N))
     ldc = _ld_2d(c, "c")
-    st = sgemm(bool(trans_a), bool(trans_b), M, N, K, float(alpha), a.data_ptr(), lda,
-               b.data_ptr(), ldb, float(beta), c.data_ptr(), ldc, _stream_handle(c))
-    _check(st, "pk_sgemm")
+    if workspace is None:
+        need = sgemm_workspace_bytes(bool(trans_a), bool(trans_b), M, N, K)
+        if need:
+            workspace = torch.empty((need + 3) // 4, dtype=torch.float32, device=a.device)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        _check_f32_cuda(workspace, "workspace")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * 4
+    st = sgemm_ws(bool(trans_a), bool(trans_b), M, N, K, float(alpha), a.data_ptr(), lda,
+                  b.data_ptr(), ldb, float(beta), c.data_ptr(), ldc, ws_ptr, ws_bytes, _stream_handle(c))
+    _check(st, "pk_sgemm_ws")
     return c
 
 
@@ -386,9 +411,13 @@ def _tune_dict(r):
     return {"config": r.config.decode(), "splits": r.splits, "ms": r.ms, "candidates": r.candidates}
 
 
-def tune_gemm(a, b, c, alpha=1.0, beta=0.0, trans_a=False, trans_b=False, iters=5):
-    """Time every compiled configuration on these operands and record the
-    fastest for this shape (see pk_tune_sgemm).  c is overwritten."""
+def tune_gemm(a, b, c, alpha=1.0, beta=0.0, trans_a=False, trans_b=False, iters=5, workspace=None):
+    """Time every compiled configuration (and reduction split the workspace
+    allows) on these operands and record the fastest for this shape (see
+    pk_tune_sgemm).  c is overwritten.  Without a workspace, one that holds
+    16 splits (at least 256 MiB, for the stream-K plans; at most 1 GiB) is
+    allocated."""
+    import torch
     _check_f32_cuda(a, "a")
     _check_f32_cuda(b, "b")
     _check_f32_cuda(c, "c")
@@ -397,9 +426,14 @@ def tune_gemm(a, b, c, alpha=1.0, beta=0.0, trans_a=False, trans_b=False, iters=
     Kb, N = (b.size(1), b.size(0)) if trans_b else (b.size(0), b.size(1))
     if Kb != K or tuple(c.shape) != (M, N):
         raise ValueError("operand shapes do not match")
+    if workspace is None:
+        need = min(max(16 * M * N * 4, 256 << 20), 1 << 30)
+        workspace = torch.empty(need // 4, dtype=torch.float32, device=a.device)
+    _check_f32_cuda(workspace, "workspace")
     r = TuneResult()
     st = load().pk_tune_sgemm(b"T" if trans_a else b"N", b"T" if trans_b else b"N", M, N, K, float(alpha),
-                              a.data_ptr(), lda, b.data_ptr(), ldb, float(beta), c.data_ptr(), ldc, int(iters),
+                              a.data_ptr(), lda, b.data_ptr(), ldb, float(beta), c.data_ptr(), ldc,
+                              workspace.data_ptr(), workspace.numel() * 4, int(iters),
                               _stream_handle(c), ctypes.byref(r))
     _check(st, "pk_tune_sgemm")
     return _tune_dict(r)

@@ -354,17 +354,37 @@ const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4)
 // (wave quantization); long reductions are split until the items fill about
 // four rounds, keeping at least 8 K-blocks per split.  Measured with the
 // automated search on the deep VGG-16 layers at batch 4 (1.13-1.22x) and the
-// 14x14x512 layer at batch 32.
+// 14x14x512 layer at batch 32.  A K-split work-group (its groups of waves
+// fill a CU) is split until the work-groups fill one round, keeping at least
+// two steps per group.
 int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 {
-    // a B-resident form's one K-block is the whole reduction; a K-split form
-    // splits K inside the work-group
-    if (c->bres || c->kgroups > 1) return 1;
+    if (c->bres) return 1;  // its one K-block is the whole reduction
     const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
     const int64_t nkb = ceil_div(K, c->bk);
-    if (tiles >= 4 * kCUs) return 1;
-    int64_t s = ceil_div(4 * kCUs, tiles);
-    const int64_t max_by_k = nkb / 8;  // keep at least 8 K-blocks per split
+    const int64_t rounds = c->kgroups > 1 ? 1 : 4;
+    if (tiles >= rounds * kCUs) return 1;
+    int64_t s = ceil_div(rounds * kCUs, tiles);
+    const int64_t max_by_k = nkb / (c->kgroups > 1 ? 2 * c->kgroups : 8);
+    if (s > max_by_k) s = max_by_k;
+    if (s > 16) s = 16;
+    return s < 1 ? 1 : (int)s;
+}
+
+// A GEMM's split of K: only when the tiles fill less than one round of the
+// CUs (a product that large is bound by its tiles' K loops, not by wave
+// quantization, and every split costs a pass over M x N partial sums), until
+// the work-groups fill about one round (K-split forms: one per CU; others:
+// two), keeping at least 8 K-blocks (K-split forms: two steps per group) per
+// split.
+int gemm_splits(const Config *c, int64_t M, int64_t N, int64_t K)
+{
+    if (c->bres) return 1;
+    const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
+    const int64_t nkb = ceil_div(K, c->bk);
+    if (tiles >= kCUs) return 1;
+    int64_t s = ceil_div((c->kgroups > 1 ? 1 : 2) * kCUs, tiles);
+    const int64_t max_by_k = nkb / (c->kgroups > 1 ? 2 * c->kgroups : 8);
     if (s > max_by_k) s = max_by_k;
     if (s > 16) s = 16;
     return s < 1 ? 1 : (int)s;
@@ -575,8 +595,9 @@ int pk_conv2d_same_pads(int64_t H, int64_t W, int64_t KH, int64_t KW, int64_t sh
     return PK_OK;
 }
 
-int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
-             int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, void *stream)
+int pk_sgemm_ws(char transA, char transB, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
+                int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, void *workspace,
+                size_t workspace_bytes, void *stream)
 {
     begin();
     const int ta = trans_flag(transA), tb = trans_flag(transB);
@@ -606,22 +627,32 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float al
     span(A, ta ? K : M, a_cols, lda, &a0, &a1);
     span(B, tb ? N : K, b_cols, ldb, &b0, &b1);
     if (overlap(c0, c1, a0, a1) || overlap(c0, c1, b0, b1)) return invalid(12);
+    if (!workspace) workspace_bytes = 0;
 
     const bool vec_ok = gemm_vec_ok(ta, tb, M, N, K, A, lda, B, ldb);
     bool bad = false;
     const Config *c = forced(&bad);
     if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
+    const bool was_forced = c != nullptr;
+    int splits = 0;  // 0: the rule's
+    SkPlan skp;
+    auto streamk_ok = [&](const Config *k) {
+        return streamk_plan(k, M, N, K, &skp) && workspace_bytes >= skp.bytes && aligned16(workspace);
+    };
     if (c) {
-        // stream-K needs a workspace, which this call does not take
-        if (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K, ldc)) return PK_ERR_NOT_SUPPORTED;
+        if (!gemm_config_fits(c, ta, tb, vec_ok) || !bres_fits(c, N, K, ldc)) return PK_ERR_NOT_SUPPORTED;
+        if (c->streamk && !streamk_ok(c)) return streamk_plan(c, M, N, K, &skp) ? PK_ERR_WORKSPACE : PK_ERR_NOT_SUPPORTED;
     } else {
         TunedShape tbuf;
         const TunedShape *t = find_tuned(0, ta, tb, M, N, K, 0, 0, &tbuf) ? &tbuf : nullptr;
         c = t ? find_config(t->config) : nullptr;
-        if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || c->streamk || !bres_fits(c, N, K, ldc))) c = nullptr;
+        if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || !bres_fits(c, N, K, ldc) || (c->streamk && !streamk_ok(c))))
+            c = nullptr;
+        if (c) splits = t->splits;
         if (!c) c = select_gemm(ta, tb, M, N, K, ldc, vec_ok);
         if (!c) return PK_ERR_NOT_SUPPORTED;
     }
+    (void)was_forced;
     KernelArgs a;
     memset(&a, 0, sizeof(a));
     a.A = A;
@@ -633,8 +664,77 @@ int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float al
     a.ldc = ldc;
     a.alpha = alpha;
     a.beta = beta;
-    fill_common(a, c, M, N, K, 1);
+    const uintptr_t w0 = (uintptr_t)workspace;
+    auto ws_overlaps = [&](size_t bytes) {
+        const uintptr_t w1 = w0 + bytes;
+        return overlap(w0, w1, a0, a1) || overlap(w0, w1, b0, b1) || overlap(w0, w1, c0, c1);
+    };
+    if (c->streamk) {
+        if (ws_overlaps(skp.bytes)) return invalid(14);
+        fill_common(a, c, M, N, K, 1);
+        a.sk_nkb = skp.nkb;
+        a.sk_groups = skp.groups;
+        a.sk_part = (float *)workspace;
+        a.sk_cnt = (int *)((char *)workspace + skp.cnt_off);
+        return launch(c, a, s);
+    }
+    const size_t per_split = (size_t)M * (size_t)N * sizeof(float);
+    if (t_forced_splits > 0) {
+        splits = t_forced_splits;
+        if (splits > 1 && c->bres) return PK_ERR_NOT_SUPPORTED;
+        if (splits > 1 && workspace_bytes < (size_t)splits * per_split) return PK_ERR_WORKSPACE;
+    } else {
+        if (splits < 1) splits = gemm_splits(c, M, N, K);
+        if (splits > 1 && workspace_bytes < (size_t)splits * per_split) splits = 1;
+    }
+    fill_common(a, c, M, N, K, splits);
+    if (a.splits > 1) {
+        if (ws_overlaps((size_t)a.splits * per_split)) return invalid(14);
+        a.ws = (float *)workspace;
+    }
     return launch(c, a, s);
+}
+
+int pk_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
+             int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, void *stream)
+{
+    return pk_sgemm_ws(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, nullptr, 0, stream);
+}
+
+size_t pk_sgemm_workspace_bytes(char transA, char transB, int64_t M, int64_t N, int64_t K)
+{
+    const int ta = trans_flag(transA), tb = trans_flag(transB);
+    if (ta < 0 || tb < 0 || M < 1 || N < 1 || K < 1) return 0;
+    if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return 0;
+    // the choice the next call on this thread makes for 16-byte aligned,
+    // tightly packed operands: a forced configuration, else the measured one,
+    // else the rules
+    const bool vec_ok = gemm_vec_ok(ta, tb, M, N, K, nullptr, ta ? M : K, nullptr, tb ? K : N);
+    bool bad = false;
+    const Config *c = forced(&bad);
+    if (bad) return 0;
+    int splits = 0;
+    if (!c) {
+        TunedShape tbuf;
+        if (find_tuned(0, ta, tb, M, N, K, 0, 0, &tbuf)) {
+            c = find_config(tbuf.config);
+            splits = tbuf.splits;
+        }
+        if (c && !gemm_config_fits(c, ta, tb, vec_ok)) c = nullptr;
+        if (!c) {
+            c = select_gemm(ta, tb, M, N, K, N, vec_ok);
+            splits = 0;
+        }
+    }
+    if (!c || !gemm_config_fits(c, ta, tb, vec_ok)) return 0;
+    if (c->streamk) {
+        SkPlan plan;
+        return streamk_plan(c, M, N, K, &plan) ? plan.bytes : 0;
+    }
+    if (t_forced_splits > 0) splits = t_forced_splits;
+    if (splits < 1) splits = gemm_splits(c, M, N, K);
+    if (c->bres || splits <= 1) return 0;
+    return (size_t)splits * (size_t)M * (size_t)N * sizeof(float);
 }
 
 size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, int64_t KH, int64_t KW,
@@ -756,7 +856,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
             if (c && !bres_fits(c, Cout, Cin, Cout)) c = nullptr;
             if (!c) c = select_gemm(0, 0, M, Cout, Cin, Cout, vec_ok);
             // a forced split needs a form that splits K across work-groups
-            if (c && t_forced_splits > 1 && (c->bres || c->kgroups > 1))
+            if (c && t_forced_splits > 1 && c->bres)
                 c = find_config(vec_ok ? "gemm_64x64x32_w2x2_nn_v44" : "gemm_64x64x16_w2x2_nn_v11");
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
@@ -839,7 +939,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     const size_t per_split = (size_t)M * (size_t)Cout * sizeof(float);
     if (t_forced_splits > 0) {
         splits = t_forced_splits;
-        if (splits > 1 && (c->bres || c->kgroups > 1)) return PK_ERR_NOT_SUPPORTED;
+        if (splits > 1 && c->bres) return PK_ERR_NOT_SUPPORTED;
         if (splits > 1 && (!workspace || workspace_bytes < (size_t)splits * per_split)) return PK_ERR_WORKSPACE;
     } else {
         const bool tuned_cfg = tuned && strcmp(c->name, tuned->config) == 0 && tuned->splits > 0;
@@ -1104,22 +1204,31 @@ void fill_result(pk_tune_result *r, const Config *c, int splits, float ms, int c
 extern "C" {
 
 int pk_tune_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
-                  int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, int iters,
-                  void *stream, pk_tune_result *result)
+                  int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, void *workspace,
+                  size_t workspace_bytes, int iters, void *stream, pk_tune_result *result)
 {
     begin();
-    if (iters < 1) return invalid(14);
-    if (!result) return invalid(16);
+    if (iters < 1) return invalid(16);
+    if (!result) return invalid(18);
     fill_result(result, nullptr, 0, 0.f, 0);
-    // validates every argument (positions as for pk_sgemm) and warms up
-    int st = pk_sgemm(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream);
+    auto call = [&] {
+        return pk_sgemm_ws(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, workspace,
+                           workspace_bytes, stream);
+    };
+    // validates every argument (positions as for pk_sgemm_ws) and warms up
+    int st = call();
     if (st != PK_OK) return st;
     if (M == 0 || N == 0 || K == 0 || alpha == 0.f) return PK_OK;  // no contraction runs
+    if (!workspace) workspace_bytes = 0;
     const int ta = trans_flag(transA), tb = trans_flag(transB);
     hipStream_t s = (hipStream_t)stream;
     EventPair ev;
     if (!ev.ok) return PK_ERR_LAUNCH;
+    // the splits tried: a fixed ladder plus each configuration's own rule
+    // split, as far as the workspace holds them
+    static const int kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16};
     const Config *best = nullptr;
+    int best_splits = 1;
     float best_ms = 0.f;
     int timed = 0;
     {
@@ -1128,24 +1237,35 @@ int pk_tune_sgemm(char transA, char transB, int64_t M, int64_t N, int64_t K, flo
         const Config *cfgs = pk::configs(&n);
         for (int i = 0; i < n; ++i) {
             const Config *c = &cfgs[i];
-            if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb || c->single_stage || c->streamk)
-                continue;
-            scope.force(c, 0);
-            const float ms = time_calls(
-                [&] { return pk_sgemm(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, stream); },
-                iters, s, ev, &st);
-            if (st == PK_ERR_LAUNCH) return st;
-            if (ms < 0.f) continue;  // this configuration does not take these operands
-            ++timed;
-            if (!best || ms < best_ms) {
-                best = c;
-                best_ms = ms;
+            if (c->kind != pk::KIND_GEMM || c->trans_a != ta || c->trans_b != tb || c->single_stage) continue;
+            int ladder[sizeof(kSplits) / sizeof(kSplits[0]) + 1];
+            int nl = 0;
+            for (int sp : kSplits) ladder[nl++] = sp;
+            const int rule = gemm_splits(c, M, N, K);
+            bool listed = false;
+            for (int j = 0; j < nl; ++j) listed = listed || ladder[j] == rule;
+            if (!listed) ladder[nl++] = rule;
+            for (int j = 0; j < nl; ++j) {
+                const int sp = ladder[j];
+                if (sp > 1 && (c->streamk || c->bres)) break;
+                if (sp > 1 && (ceil_div(K, c->bk) < sp || workspace_bytes < (size_t)sp * M * N * sizeof(float)))
+                    continue;
+                scope.force(c, sp);
+                const float ms = time_calls(call, iters, s, ev, &st);
+                if (st == PK_ERR_LAUNCH) return st;
+                if (ms < 0.f) break;  // this configuration does not take these operands
+                ++timed;
+                if (!best || ms < best_ms) {
+                    best = c;
+                    best_splits = sp;
+                    best_ms = ms;
+                }
             }
         }
     }
     if (!best) return PK_ERR_NOT_SUPPORTED;
-    if (!record_tuned({0, ta, tb, M, N, K, 0, 0, best->name, 0})) return PK_ERR_NOT_SUPPORTED;
-    fill_result(result, best, 1, best_ms, timed);
+    if (!record_tuned({0, ta, tb, M, N, K, 0, 0, best->name, best_splits})) return PK_ERR_NOT_SUPPORTED;
+    fill_result(result, best, best_splits, best_ms, timed);
     t_last_param = 0;
     t_last_config = best->name;
     return PK_OK;
@@ -1198,7 +1318,7 @@ int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t 
             if (!listed) ladder[nl++] = rule;
             for (int j = 0; j < nl; ++j) {
                 const int sp = ladder[j];
-                if (sp > 1 && (c->kind == pk::KIND_DIRECT || c->streamk || c->bres || c->kgroups > 1)) break;
+                if (sp > 1 && (c->kind == pk::KIND_DIRECT || c->streamk || c->bres)) break;
                 if (sp > 1 && workspace_bytes < (size_t)sp * M * Cout * sizeof(float)) continue;
                 scope.force(c, sp);
                 const float ms = time_calls(call, iters, s, ev, &st);

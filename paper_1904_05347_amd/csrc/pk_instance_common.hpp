@@ -128,14 +128,13 @@ static hipError_t launch_gemm_bres(const KernelArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
-// K split among KS groups of waves inside each work-group (one work-group per
-// tile, no split across work-groups).
+// K split among KS groups of waves inside each work-group; a split across
+// work-groups (grid z) divides the K-blocks first, as in launch_gemm.
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int KS, int AHEAD, int AMODE, bool B_KCONTIG, int VA,
           int VB, int OCC>
 static hipError_t launch_gemm_ksplit(const KernelArgs &a, hipStream_t stream)
 {
-    if (a.splits > 1) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), 1);
+    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
     const dim3 block(64 * WAVES_M * WAVES_N * KS);
     if (reads_c<AMODE>(a)) {
         hipLaunchKernelGGL(

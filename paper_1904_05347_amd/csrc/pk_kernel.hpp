@@ -725,25 +725,27 @@ gemm_ksplit_kernel(KernelArgs p)
     int tm, tn;
     tile_coords(p, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
-    const int nkb = (p.K + BK - 1) / BK;
-    const int steps = (nkb + KS - 1) / KS;  // K-block steps of every group
+    int kbeg, kend;  // K-blocks of this work-group's split
+    split_range(p, BK, blockIdx.z, kbeg, kend);
+    const int steps = (kend - kbeg + KS - 1) / KS;  // K-block steps of every group
+    const int klim = min(p.K, kend * BK);          // k past the split reads as zero
 
     ALoader la;
     BLoader lb;
-    la.init(p.A, p.lda, m0, p.M, grp, tid);
-    lb.init(p.B, p.ldb, n0, p.N, grp, tid);
+    la.init(p.A, p.lda, m0, p.M, kbeg + grp, tid);
+    lb.init(p.B, p.ldb, n0, p.N, kbeg + grp, tid);
 
     typename G::Acc acc;
     G::zero(acc);
     typename ALoader::VT ra0[ALoader::LOADS], ra1[AHEAD == 2 ? ALoader::LOADS : 1];
     typename BLoader::VT rb0[BLoader::LOADS], rb1[AHEAD == 2 ? BLoader::LOADS : 1];
 
-    // step st of group g multiplies K-block st*KS + g (zeros past the end:
-    // the loaders read nothing at k >= K); steps are fetched in order
+    // step st of group g multiplies K-block kbeg + st*KS + g (zeros past the
+    // split: the loaders read nothing at k >= klim); steps are fetched in order
     auto fetch = [&](typename ALoader::VT *ra, typename BLoader::VT *rb, int st) {
-        const int k0 = (st * KS + grp) * BK;
-        la.load(ra, k0, p.K, tid);
-        lb.load(rb, k0, p.K, tid);
+        const int k0 = (kbeg + st * KS + grp) * BK;
+        la.load(ra, k0, klim, tid);
+        lb.load(rb, k0, klim, tid);
         la.advance_by(KS);
         lb.advance_by(KS);
     };
@@ -823,7 +825,7 @@ gemm_ksplit_kernel(KernelArgs p)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) acc[i][j][r] += slot[((i * G::RN + j) * 16 + r) * GT];
         }
-        G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, 0);
+        G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
     }
 }
 

@@ -155,17 +155,61 @@ def test_winograd_argument_checks(pk):
     assert call(N=0) == 0
 
 
+def test_gemm_workspace_checks(pk):
+    """pk_sgemm_ws: a forced split needs workspace for every slice
+    (PK_ERR_WORKSPACE), the workspace must not overlap A, B or C (position 14),
+    a B-resident form takes no split; the size query follows the forced
+    choice and the rules.  Every call fails before a kernel launches."""
+    from paper_1904_05347_amd import binding
+    fake = 0x100000
+    M, N, K = 64, 64, 1024
+    A, B, C = fake, fake + (1 << 22), fake + (2 << 22)
+    ws = fake + (4 << 22)
+    per_split = M * N * 4
+
+    def call(ws_ptr, ws_bytes):
+        st = binding.sgemm_ws("N", "N", M, N, K, 1.0, A, K, B, N, 0.0, C, N, ws_ptr, ws_bytes)
+        return st, pk.last_invalid_param()
+
+    pk.force_config("gemm_64x64x32_w2x2_nn_v44")
+    pk.force_splits(4)
+    try:
+        assert binding.sgemm_workspace_bytes("N", "N", M, N, K) == 4 * per_split
+        assert call(None, 0)[0] == 3
+        assert call(ws, 4 * per_split - 4)[0] == 3
+        assert call(A + 64, 4 * per_split) == (1, 14)
+        assert call(C - 4 * per_split + 4, 4 * per_split) == (1, 14)
+    finally:
+        pk.force_config(None)
+        pk.force_splits(0)
+    pk.force_config("gemm_64x64x64_w2x2_nn_v44_br")
+    pk.force_splits(2)
+    try:
+        st = binding.sgemm_ws("N", "N", M, N, 64, 1.0, A, 64, B, N, 0.0, C, N, ws, 2 * per_split)
+        assert st == 2
+    finally:
+        pk.force_config(None)
+        pk.force_splits(0)
+    # the rules: a product whose tiles fill the CUs takes no split; a small
+    # one with a long K takes one (K-split form, at least two steps per group)
+    assert binding.sgemm_workspace_bytes("N", "N", 4096, 4096, 4096) == 0
+    assert binding.sgemm_workspace_bytes("N", "N", 64, 64, 64) == 0
+    need = binding.sgemm_workspace_bytes("N", "N", 64, 64, 1024)
+    assert need > 0 and need % per_split == 0
+
+
 def test_tune_argument_checks(pk):
     """The tuner's own arguments are checked before anything runs."""
     from paper_1904_05347_amd import binding
     lib = pk.load()
     fake = 0x10000
     r = binding.TuneResult()
-    st = lib.pk_tune_sgemm(b"N", b"N", 8, 8, 8, 1.0, fake, 8, fake + 4096, 8, 0.0, fake + 8192, 8, 0, None,
-                           ctypes.byref(r))
-    assert (st, pk.last_invalid_param()) == (1, 14)
-    st = lib.pk_tune_sgemm(b"N", b"N", 8, 8, 8, 1.0, fake, 8, fake + 4096, 8, 0.0, fake + 8192, 8, 3, None, None)
+    st = lib.pk_tune_sgemm(b"N", b"N", 8, 8, 8, 1.0, fake, 8, fake + 4096, 8, 0.0, fake + 8192, 8, None, 0, 0,
+                           None, ctypes.byref(r))
     assert (st, pk.last_invalid_param()) == (1, 16)
+    st = lib.pk_tune_sgemm(b"N", b"N", 8, 8, 8, 1.0, fake, 8, fake + 4096, 8, 0.0, fake + 8192, 8, None, 0, 3,
+                           None, None)
+    assert (st, pk.last_invalid_param()) == (1, 18)
     conv = [fake, 1, 5, 5, 4, fake + (1 << 20), 3, 3, 4, 1, 1, 1, 1, 1, 1, fake + (2 << 20), 5, 5, None, 0]
     st = lib.pk_tune_conv2d_fwd(*conv, 0, None, ctypes.byref(r))
     assert (st, pk.last_invalid_param()) == (1, 21)

@@ -164,6 +164,65 @@ def test_every_gemm_config_forced():
             assert np.array_equal(out.astype(np.float64), ref), (cfg["name"], M, N, K)
 
 
+def test_gemm_workspace_splits_and_streamk():
+    """pk_sgemm_ws: every GEMM configuration that splits K across
+    work-groups (tiled, persistent, K-split forms: forced splits of 2 and 3,
+    the last slice ragged) and every stream-K form, on integer data with
+    beta = 0.5: the slices added in a fixed order must equal the oracle bit
+    for bit, twice in a row (a workspace reused with stale contents)."""
+    torch, pk = require_gpu()
+    ran = 0
+    ws = torch.empty(256 << 18, dtype=torch.float32, device="cuda")  # 256 MiB
+    for cfg in pk.configs():
+        if cfg["kind"] != 0 or cfg["bres"]:
+            continue
+        ta = "T" if cfg["trans_a"] else "N"
+        tb = "T" if cfg["trans_b"] else "N"
+        for M, N, K in [(132, 68, 1000), (36, 200, 92)]:
+            rng = np.random.default_rng(M * 5 + N + K)
+            A = wl.integers(rng, M * K).reshape((K, M) if ta == "T" else (M, K))
+            B = wl.integers(rng, K * N).reshape((N, K) if tb == "T" else (K, N))
+            C = wl.integers(rng, M * N).reshape(M, N)
+            ref, _ = oracle.sgemm(ta, tb, M, N, K, 1.0, A, A.shape[1], B, B.shape[1], 0.5, C, N)
+            dA, dB = dev(A), dev(B)
+            for splits in ((0,) if cfg["streamk"] else (2, 3)):
+                for rep in range(2):
+                    dC = dev(C)
+                    pk.force_config(cfg["name"])
+                    pk.force_splits(splits)
+                    try:
+                        st = pk.binding.sgemm_ws(ta, tb, M, N, K, 1.0, dA.data_ptr(), A.shape[1], dB.data_ptr(),
+                                                 B.shape[1], 0.5, dC.data_ptr(), N, ws.data_ptr(), ws.numel() * 4)
+                        used = pk.last_config_name()
+                    finally:
+                        pk.force_config(None)
+                        pk.force_splits(0)
+                    if st == 2:  # this configuration does not take these operands
+                        break
+                    assert st == 0 and used == cfg["name"], (cfg["name"], st)
+                    assert np.array_equal(host(dC).astype(np.float64), ref), (cfg["name"], M, N, K, splits, rep)
+                    ran += 1
+    assert ran >= 400
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 64, 1024), (1024, 64, 512), (256, 1024, 1024), (100, 36, 2000)])
+def test_gemm_default_workspace(M, N, K):
+    """The default choice with the workspace the binding allocates (a split
+    across work-groups for these few-tile, long-K products) against the
+    oracle on random data."""
+    torch, pk = require_gpu()
+    need = pk.binding.sgemm_workspace_bytes("N", "N", M, N, K)
+    assert need > 0
+    rng = np.random.default_rng(M + 3 * N + K)
+    A = wl.uniform(rng, M * K).reshape(M, K)
+    B = wl.uniform(rng, K * N).reshape(K, N)
+    C = wl.uniform(rng, M * N).reshape(M, N)
+    dC = dev(C)
+    pk.gemm(dev(A), dev(B), dC, alpha=1.5, beta=-0.5)
+    ref, scale = oracle.sgemm("N", "N", M, N, K, 1.5, A, K, B, N, -0.5, C, N)
+    assert_parity(host(dC), ref, scale, "gemm %dx%dx%d %s" % (M, N, K, pk.last_config_name()))
+
+
 def test_ksplit_configs():
     """K split among groups of waves inside the work-group: a long reduction
     that does not divide into the groups' K-blocks (groups past the end add
@@ -262,7 +321,8 @@ def test_paper_gemm_sweep(case):
 
 def test_streamk_configs_refused_by_sgemm():
     """Stream-K needs a workspace, which pk_sgemm does not take: a forced
-    stream-K configuration is refused with PK_ERR_NOT_SUPPORTED."""
+    stream-K configuration is refused with PK_ERR_WORKSPACE (as pk_sgemm_ws
+    with none)."""
     torch, pk = require_gpu()
     name = next(c["name"] for c in pk.configs() if c["streamk"] and c["kind"] == 0)
     a = torch.ones((64, 64), dtype=torch.float32, device="cuda")
@@ -272,7 +332,7 @@ def test_streamk_configs_refused_by_sgemm():
         st = pk.binding.sgemm("N", "N", 64, 64, 64, 1.0, a.data_ptr(), 64, a.data_ptr(), 64, 0.0, c.data_ptr(), 64)
     finally:
         pk.force_config(None)
-    assert st == 2
+    assert st == 3
 
 
 def test_bres_configs():
