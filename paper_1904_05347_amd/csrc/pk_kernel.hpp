@@ -1314,11 +1314,19 @@ gemm_bres_kernel(KernelArgs p)
     const int t1 = (int)(((int64_t)(rg + 1) * tiles) / groups);
     if (t0 >= t1) return;  // uniform over the work-group, before any barrier
 
-    // B: BK x BN row-major in global memory -> Bs[n][k]
+    // B: BK x BN row-major in global memory -> Bs[n][k].  Chunk c (4 columns
+    // of one row) goes to a lane so that a wave covers 16 consecutive k of 4
+    // adjacent column chunks: its transposed writes then fall in 64 distinct
+    // banks (4 columns apart is 4 * (BK + 4) = 16 mod 64 banks), and its
+    // global reads are 64-byte runs of 16 rows.  (Consecutive lanes on
+    // consecutive column chunks would land a wave's writes in 4 banks.)
+    static_assert(BK % 16 == 0 && BN % 16 == 0, "B staging by 16 k x 4 chunks");
 #pragma unroll
     for (int i = 0; i < BK * BN / 4 / NT; ++i) {
         const int c = tid + i * NT;
-        const int k = c / (BN / 4), n = (c % (BN / 4)) * 4;
+        const int rest = c / 64;
+        const int k = (rest % (BK / 16)) * 16 + c % 16;
+        const int n = ((rest / (BK / 16)) * 4 + (c / 16) % 4) * 4;
         const f32x4 v = *reinterpret_cast<const f32x4 *>(p.B + (int64_t)k * p.ldb + n0 + n);
         Bs[(n + 0) * G::LDB_S + k] = v[0];
         Bs[(n + 1) * G::LDB_S + k] = v[1];
