@@ -263,7 +263,7 @@ typedef struct {
     int threads;     /* work-group size */
     int trans_a, trans_b; /* operand layouts read (1 = transposed storage) */
     int vec_a, vec_b; /* elements per global load */
-    int stages;      /* LDS buffers (2 = double buffered) */
+    int stages;      /* LDS buffers (2 = double buffered, 3 = two K-blocks in flight) */
     int lds_bytes;   /* LDS per work-group */
     int occupancy;   /* waves per SIMD its registers are allotted for (1 = unconstrained) */
     int persistent;  /* 1 = one work-group per resident slot, each looping over tiles */
@@ -273,6 +273,8 @@ typedef struct {
                         only products with K == bk and N == bn (op(A) = A, op(B) = B) */
     int kgroups;     /* groups of waves splitting K inside one work-group (1 = none); their
                         partial tiles are added through LDS in group order */
+    int dma;         /* 1 = operands copied straight from global memory into LDS (no
+                        staging registers, unpadded swizzled tiles, `stages` of them) */
 } pk_config_info;
 
 int pk_num_configs(void);

@@ -47,7 +47,7 @@ class ConfigInfo(ctypes.Structure):
                 ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
                 ("stages", ctypes.c_int), ("lds_bytes", ctypes.c_int), ("occupancy", ctypes.c_int),
                 ("persistent", ctypes.c_int), ("streamk", ctypes.c_int),
-                ("bres", ctypes.c_int), ("kgroups", ctypes.c_int)]
+                ("bres", ctypes.c_int), ("kgroups", ctypes.c_int), ("dma", ctypes.c_int)]
 
 
 class TuneResult(ctypes.Structure):

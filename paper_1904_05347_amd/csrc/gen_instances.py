@@ -76,6 +76,13 @@ KSPLIT = [(64, 64, 16, 2, 2, 4, 1, 4, 4, 1), (64, 64, 32, 2, 2, 4, 1, 4, 4, 1), 
           (64, 64, 16, 2, 2, 4, 2, 4, 4, 1), (64, 64, 32, 2, 2, 4, 2, 4, 4, 1), (64, 64, 32, 2, 2, 2, 2, 4, 4, 1),
           (32, 64, 32, 1, 2, 4, 2, 4, 4, 1), (32, 64, 16, 1, 2, 8, 2, 4, 4, 1)]
 
+# Direct-to-LDS staging ("_dmaS", S LDS stages; NN, TN, NT): the
+# register-staged loader's alternative, beside the same tiles.  (BM, BN, BK, WAVES_M, WAVES_N,
+# stages, OCC)
+DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2, 4, 4, 2),
+       (128, 128, 32, 2, 4, 2, 2), (128, 128, 32, 2, 4, 3, 2), (128, 128, 32, 2, 4, 4, 2),
+       (128, 128, 16, 2, 2, 3, 1), (128, 128, 16, 2, 2, 4, 1), (64, 64, 32, 2, 2, 3, 1)]
+
 # TT only needs a large, a small and a scalar-load tile.
 TT_TILES = [(128, 128, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 1, 1, 1)]
 
@@ -175,6 +182,12 @@ def main():
                            % ("gemm_%dx%dx%d_w%dx%d_k%d_%s_v%d%d%s" % (bm, bn, bk, wm, wn, ks, layout, va, vb,
                                                                     "_d2" if ahead == 2 else ""),
                               bm, bn, bk, wm, wn, ks, ahead, ta, tb, va, vb, occ))
+        for t in (DMA if layout != "tt" else []):
+            bm, bn, bk, wm, wn, st, occ = t
+            entries.append("PK_GEMM_DMA(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
+                           % ("gemm_%dx%dx%d_w%dx%d_%s_v44%s_dma%d" % (bm, bn, bk, wm, wn, layout,
+                                                                     "_o%d" % occ if occ > 1 else "", st),
+                              bm, bn, bk, wm, wn, st, ta, tb, occ))
         for t in (DEEP if layout == "nn" else []):
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM_D(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"

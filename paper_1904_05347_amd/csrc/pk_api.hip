@@ -150,9 +150,9 @@ struct TunedShape {
 };
 
 const TunedShape kTuned[] = {
-    {0, 0, 0, 4096, 4096, 4096, 0, 0, "gemm_256x256x16_w2x4_nn_v44_o2", 0},
-    {0, 1, 0, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_tn_v44_o2", 0},
-    {0, 0, 1, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_nt_v44_o2", 0},
+    {0, 0, 0, 4096, 4096, 4096, 0, 0, "gemm_128x128x32_w2x4_nn_v44_o2_dma2", 0},
+    {0, 1, 0, 4096, 4096, 4096, 0, 0, "gemm_128x128x32_w2x4_tn_v44_o2_dma2", 0},
+    {0, 0, 1, 4096, 4096, 4096, 0, 0, "gemm_256x256x16_w2x4_nt_v44_o2_dma4", 0},
     {0, 0, 0, 2048, 2048, 2048, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
     // VGG-16 block-first layers at batch 32 (3x3, stride 1)
     {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
@@ -281,6 +281,17 @@ bool bres_fits(const Config *c, int64_t N, int64_t K, int64_t ldc)
 {
     return !c->bres || (N % c->bn == 0 && K == c->bk &&
                         (int64_t)(c->bm + 1) * ldc * (int64_t)sizeof(float) < ((int64_t)1 << 31));
+}
+
+// A direct-to-LDS configuration addresses the rows of one tile of each
+// operand (BM or BK of A, BK or BN of B, by layout) from one base in 32-bit
+// byte offsets.
+bool dma_fits(const Config *c, int64_t lda, int64_t ldb)
+{
+    const int64_t lim = (int64_t)1 << 31;
+    const int64_t a_rows = c->trans_a ? c->bk : c->bm, a_cols = c->trans_a ? c->bm : c->bk;
+    const int64_t b_rows = c->trans_b ? c->bn : c->bk, b_cols = c->trans_b ? c->bk : c->bn;
+    return !c->dma || (a_rows * lda * 4 + a_cols * 4 < lim && b_rows * ldb * 4 + b_cols * 4 < lim);
 }
 
 // Shapes outside the table, from the same measurements:
@@ -529,13 +540,14 @@ int pk_get_config(int idx, pk_config_info *info)
     info->trans_b = c->trans_b;
     info->vec_a = c->vec_a;
     info->vec_b = c->vec_b;
-    info->stages = c->single_stage ? 1 : 2;
+    info->stages = c->dma ? c->dma : (c->single_stage ? 1 : 2);
     info->lds_bytes = c->lds_bytes;
     info->occupancy = c->occupancy;
     info->persistent = c->persistent;
     info->streamk = c->streamk;
     info->bres = c->bres;
     info->kgroups = c->kgroups;
+    info->dma = c->dma ? 1 : 0;
     return PK_OK;
 }
 
@@ -640,13 +652,15 @@ int pk_sgemm_ws(char transA, char transB, int64_t M, int64_t N, int64_t K, float
         return streamk_plan(k, M, N, K, &skp) && workspace_bytes >= skp.bytes && aligned16(workspace);
     };
     if (c) {
-        if (!gemm_config_fits(c, ta, tb, vec_ok) || !bres_fits(c, N, K, ldc)) return PK_ERR_NOT_SUPPORTED;
+        if (!gemm_config_fits(c, ta, tb, vec_ok) || !bres_fits(c, N, K, ldc) || !dma_fits(c, lda, ldb))
+            return PK_ERR_NOT_SUPPORTED;
         if (c->streamk && !streamk_ok(c)) return streamk_plan(c, M, N, K, &skp) ? PK_ERR_WORKSPACE : PK_ERR_NOT_SUPPORTED;
     } else {
         TunedShape tbuf;
         const TunedShape *t = find_tuned(0, ta, tb, M, N, K, 0, 0, &tbuf) ? &tbuf : nullptr;
         c = t ? find_config(t->config) : nullptr;
-        if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || !bres_fits(c, N, K, ldc) || (c->streamk && !streamk_ok(c))))
+        if (c && (!gemm_config_fits(c, ta, tb, vec_ok) || !bres_fits(c, N, K, ldc) || !dma_fits(c, lda, ldb) ||
+                  (c->streamk && !streamk_ok(c))))
             c = nullptr;
         if (c) splits = t->splits;
         if (!c) c = select_gemm(ta, tb, M, N, K, ldc, vec_ok);
@@ -850,10 +864,11 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     const bool vb4 = Cout % 4 == 0 && aligned16(f);
     if (gemm_path) {
         if (c) {
-            if (!gemm_config_fits(c, 0, 0, vec_ok) || !bres_fits(c, Cout, Cin, Cout)) return PK_ERR_NOT_SUPPORTED;
+            if (!gemm_config_fits(c, 0, 0, vec_ok) || !bres_fits(c, Cout, Cin, Cout) || !dma_fits(c, Cin, Cout))
+                return PK_ERR_NOT_SUPPORTED;
         } else {
             c = (tuned && vec_ok) ? find_config(tuned->config) : nullptr;
-            if (c && !bres_fits(c, Cout, Cin, Cout)) c = nullptr;
+            if (c && (!bres_fits(c, Cout, Cin, Cout) || !dma_fits(c, Cin, Cout))) c = nullptr;
             if (!c) c = select_gemm(0, 0, M, Cout, Cin, Cout, vec_ok);
             // a forced split needs a form that splits K across work-groups
             if (c && t_forced_splits > 1 && c->bres)
@@ -1001,7 +1016,7 @@ const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok
     (void)Cout;
     const Config *c = forced(bad);
     if (*bad) return nullptr;
-    if (c) return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent && !c->streamk && !c->bres) ? c : nullptr;
+    if (c) return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent && !c->streamk && !c->bres && !c->dma) ? c : nullptr;
     if (!vec_ok) return find_config("gemm_64x64x16_w2x2_nn_v11");
     return find_config(Cin <= 128 ? "gemm_64x64x16_w2x2_nn_v44" : "gemm_64x64x32_w2x2_nn_v44");
 }

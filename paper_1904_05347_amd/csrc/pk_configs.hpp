@@ -36,6 +36,7 @@ struct Config {
     int (*resident)(int beta);
     int bres;  // 1 = op(B) resident in LDS: runs only products with K == bk and N a multiple of bn
     int kgroups = 1;  // groups of waves splitting K inside the work-group (gemm_ksplit_kernel)
+    int dma = 0;      // LDS stages filled straight from global memory (gemm_dma_kernel); 0 = register-staged
 };
 
 // The registry (defined with the kernel instances, host side only).

@@ -147,6 +147,23 @@ static hipError_t launch_gemm_ksplit(const KernelArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
+// Direct-to-LDS staging (same grid as launch_gemm; dense operands).  The
+// host checks that the rows one tile addresses span less than 2 GiB.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, bool TA, bool TB, int OCC>
+static hipError_t launch_gemm_dma(const KernelArgs &a, hipStream_t stream)
+{
+    const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
+    const dim3 block(64 * WAVES_M * WAVES_N);
+    if (reads_c<A_KCONTIG>(a)) {
+        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, TA, TB, OCC, true>), grid, block, 0,
+                           stream, a);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, TA, TB, OCC, false>), grid, block, 0,
+                       stream, a);
+    return hipGetLastError();
+}
+
 // Loads two K-blocks ahead (same grid as launch_gemm).
 template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int AMODE, bool B_KCONTIG, int VA, int VB, int OCC>
 static hipError_t launch_gemm_deep(const KernelArgs &a, hipStream_t stream)
@@ -219,6 +236,10 @@ static constexpr int lds_bytes()
      KS * lds_bytes<BM, BN, BK, WM, WN, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB>(),           \
      &launch_gemm_ksplit<BM, BN, BK, WM, WN, KS, AHEAD, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), VA, VB, OCC>, \
      0, 0, nullptr, 0, KS}
+
+#define PK_GEMM_DMA(name, BM, BN, BK, WM, WN, STAGES, TA, TB, OCC)                                    \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, 4, 4, OCC, 0, STAGES * 4 * (BM * BK + BK * BN),     \
+     &launch_gemm_dma<BM, BN, BK, WM, WN, STAGES, (TA != 0), (TB != 0), OCC>, 0, 0, nullptr, 0, 1, STAGES}
 
 #define PK_CONV_D(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                               \
     {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 0,                                      \

@@ -573,6 +573,203 @@ gemm_kernel(KernelArgs p)
     G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
 }
 
+// One operand tile copied straight from global memory into LDS by
+// buffer_load_dwordx4 ... lds (no staging registers, no LDS write
+// instructions).  One such instruction fills 1 KiB of LDS contiguously (lane
+// i at base + 16 i), so the tile cannot carry the row padding the
+// register-staged loaders use against bank conflicts; chunk positions are
+// XOR-swizzled instead.
+//   KROWS (A 'N', B 'T'): R x BK, rows of contiguous k, CPR 16-byte chunks
+//     per row; chunk c of row r sits at position c ^ ((r / (16 / CPR)) %
+//     CPR), so the 16 rows one ds_read_b128 pass touches fall in 16
+//     distinct bank quads.
+//   k-major (A 'T', B 'N'): BK x R, rows of contiguous m (n); the second
+//     half of the K-block (read by lanes 32..63) has its chunks XOR 8, i.e.
+//     column x sits at x ^ 32, so the two half-waves' 128-byte reads use
+//     opposite halves of the 64 banks.
+// Elements past the operand's rows or K get an offset past the buffer's
+// range, which the hardware answers with zeros.  Offsets count from a
+// per-tile, per-K-block base, so they stay below 2^31 whenever R (KROWS) or
+// BK (k-major) rows of the operand do (checked by the host).
+template <int R, int BK, int NW, bool KROWS>
+struct DmaOperand {
+    static constexpr int CPR = KROWS ? BK / 4 : R / 4;  // 16-byte chunks per LDS row
+    static constexpr int RPS = KROWS ? 16 / CPR : 1;    // rows per step of the KROWS swizzle
+    static constexpr int FLOATS = R * BK;
+    static constexpr int L = FLOATS / 256 / NW;  // instructions per lane per K-block
+    static_assert(FLOATS % (256 * NW) == 0, "whole 1 KiB pieces per wave");
+    static_assert(KROWS ? (CPR <= 16 && 16 % CPR == 0) : (R % 64 == 0), "swizzle geometry");
+    int off[L], kk[L];
+    bool ok[L];
+
+    // ld: the operand's leading dimension; r0 / rlim: its first row (m or
+    // n) of this tile and the row count
+    __device__ __forceinline__ void init(int64_t ld, int r0, int rlim, int wave, int lane)
+    {
+#pragma unroll
+        for (int i = 0; i < L; ++i) {
+            const int q = (i * NW + wave) * 64 + lane;  // chunk position in the tile
+            if constexpr (KROWS) {
+                const int r = q / CPR;
+                const int c = (q % CPR) ^ ((r / RPS) % CPR);
+                off[i] = (r * (int)ld + 4 * c) * 4;
+                kk[i] = 4 * c;
+                ok[i] = r0 + r < rlim;
+            } else {
+                const int k = q / CPR;
+                const int c = (q % CPR) ^ (k >= BK / 2 ? 8 : 0);
+                off[i] = (k * (int)ld + 4 * c) * 4;
+                kk[i] = k;
+                ok[i] = r0 + 4 * c < rlim;
+            }
+        }
+    }
+    // copy K-block k0 of the tile whose rows start at r0 into `tile`
+    __device__ __forceinline__ void issue(const float *base, int64_t ld, int r0, int k0, int K, float *tile,
+                                          int wave) const
+    {
+        const float *b = KROWS ? base + (int64_t)r0 * ld + k0 : base + (int64_t)k0 * ld + r0;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)b, 0, 0x7fffffff, 0x00020000);
+#pragma unroll
+        for (int i = 0; i < L; ++i) {
+            const int o = (ok[i] && k0 + kk[i] < K) ? off[i] : (int)0x80000000;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs, (__attribute__((address_space(3))) void *)(tile + (i * NW + wave) * 256), 16, o, 0, 0, 0);
+        }
+    }
+    // the four k (h*BK/2 + 4g + t, t = 0..3) of row `row` for MFMA group g
+    __device__ __forceinline__ static void read4(const float *tile, int row, int h, int g, float *v)
+    {
+        if constexpr (KROWS) {
+            const int c = h * (BK / 8) + g;
+            const f32x4 x = *reinterpret_cast<const f32x4 *>(tile + row * BK + 4 * (c ^ ((row / RPS) % CPR)));
+            v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+        } else {
+            const int k = h * (BK / 2) + 4 * g;
+            const int col = row ^ (32 * h);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) v[t] = tile[(k + t) * R + col];
+        }
+    }
+};
+
+// The contraction (dense operands, any of the four layouts) with both
+// operand tiles copied straight into STAGES LDS stages (DmaOperand): S-1
+// K-blocks are in flight at no register cost.  The compiler does not see
+// these writes to LDS, so every wait for them is explicit and followed by a
+// compiler memory barrier, and the work-group barrier is issued without
+// __syncthreads()'s fence (which would also wait for the copies in flight
+// for later blocks).  Same MFMA group pipeline as gemm_kernel.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, bool TA, bool TB, int OCC, bool BETA>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_dma_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, false, 4, 4> G;  // MFMA and epilogue only
+    constexpr int NW = G::NT / 64;
+    typedef DmaOperand<BM, BK, NW, !TA> OpA;
+    typedef DmaOperand<BN, BK, NW, TB> OpB;
+    constexpr int A_ST = OpA::FLOATS, B_ST = OpB::FLOATS;  // floats per stage
+    constexpr int LPB = OpA::L + OpB::L;                    // copies per lane per K-block
+    static_assert(STAGES >= 2 && STAGES <= 4, "two to four LDS stages");
+    static_assert((STAGES - 2) * LPB <= 63, "vmcnt range");
+
+    __shared__ __attribute__((aligned(16))) float smem[STAGES * (A_ST + B_ST)];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+
+    {  // product blockIdx.y of a batch
+        const int64_t bz = blockIdx.y;
+        p.A += bz * p.stride_a;
+        p.B += bz * p.stride_b;
+        p.C += bz * p.stride_c;
+    }
+    int tm, tn;
+    tile_coords(p, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    int kbeg, kend;
+    split_range(p, BK, blockIdx.z, kbeg, kend);
+
+    OpA oa;
+    OpB ob;
+    oa.init(p.lda, m0, p.M, wave, lane);
+    ob.init(p.ldb, n0, p.N, wave, lane);
+    auto issue = [&](int kb, int s) {
+        float *as = smem + s * (A_ST + B_ST);
+        oa.issue(p.A, p.lda, m0, kb * BK, p.K, as, wave);
+        ob.issue(p.B, p.ldb, n0, kb * BK, p.K, as + A_ST, wave);
+    };
+    // wait until this lane's copies of every issued block but the newest
+    // `later` ones (0 .. STAGES-2) have landed in LDS
+    auto wait_blocks = [&](int later) {
+        if (STAGES >= 4 && later >= 2)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPB) : "memory");
+        else if (STAGES >= 3 && later >= 1)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPB) : "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+    // this wave's LDS reads are complete (no copy issued after the barrier
+    // can overwrite what they still fetch) and its copies for the block about
+    // to be read have landed (wait_blocks), so the barrier alone publishes
+    // the stage
+    auto barrier = [] {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    auto read_group = [&](const float *as, int g, typename G::FragA &xa, typename G::FragB &xb) {
+#pragma unroll
+        for (int i = 0; i < G::RM; ++i) OpA::read4(as, a_row + i * 32, h, g, xa[i]);
+#pragma unroll
+        for (int j = 0; j < G::RN; ++j) OpB::read4(as + A_ST, b_row + j * 32, h, g, xb[j]);
+    };
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NG = G::NG;
+
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (kbeg + s < kend) issue(kbeg + s, s);
+    wait_blocks(min(STAGES - 2, kend - kbeg - 1));
+    barrier();
+    if (kbeg < kend) read_group(smem, 0, fa[0], fb[0]);
+
+    // Block kb sits in stage s.  At the top the copy of block kb+S-1 goes
+    // into the stage block kb-1 used (all of its reads are behind the
+    // barrier that ended block kb-1); block kb+1 is waited for before the
+    // barrier that ends block kb.
+    int s = 0;
+    for (int kb = kbeg; kb < kend; ++kb) {
+        const int s_next = s + 1 == STAGES ? 0 : s + 1;
+        if (kb + STAGES - 1 < kend) issue(kb + STAGES - 1, s == 0 ? STAGES - 1 : s - 1);
+        const float *as = smem + s * (A_ST + B_ST);
+#pragma unroll
+        for (int g = 0; g < NG - 1; ++g) {
+            read_group(as, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        wait_blocks(min(STAGES - 2, kend - kb - 2));
+        barrier();
+        // unconditional (stale after the last block, never used)
+        read_group(smem + s_next * (A_ST + B_ST), 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
+        s = s_next;
+    }
+
+    G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+}
+
 // The same contraction with the global loads TWO K-blocks ahead: two
 // register sets alternate, so the loads of block kb+2 are issued while block
 // kb multiplies and are stored to LDS only at the end of block kb+1.  Each

@@ -231,6 +231,11 @@ def test_config_space(pk):
             continue
         assert c["bm"] % (32 * c["waves_m"]) == 0 and c["bn"] % (32 * c["waves_n"]) == 0
         assert c["bk"] % 8 == 0
+        if c["dma"]:  # unpadded, swizzled tiles copied straight into 2 to 4 LDS stages
+            assert c["kind"] == 0 and c["stages"] in (2, 3, 4) and c["vec_a"] == c["vec_b"] == 4
+            assert c["lds_bytes"] == c["stages"] * 4 * (c["bm"] * c["bk"] + c["bk"] * c["bn"]), c["name"]
+            assert c["name"].endswith("_dma%d" % c["stages"])
+            continue
         assert c["stages"] in (1, 2)
         assert c["stages"] == 2 or (c["kind"] == 0 and c["name"].endswith("_s1"))
         # one or two LDS stages of the A and B tiles, each row padded by 4 floats
