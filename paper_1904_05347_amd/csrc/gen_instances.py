@@ -83,6 +83,9 @@ DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2,
        (128, 128, 32, 2, 4, 2, 2), (128, 128, 32, 2, 4, 3, 2), (128, 128, 32, 2, 4, 4, 2),
        (128, 128, 16, 2, 2, 3, 1), (128, 128, 16, 2, 2, 4, 1), (64, 64, 32, 2, 2, 3, 1)]
 
+# Stream-K forms of the direct-to-LDS contraction (NN GEMM and convolution).
+DMA_STREAMK = [(128, 128, 32, 2, 4, 2, 2), (128, 128, 16, 2, 2, 3, 1), (128, 128, 32, 2, 4, 3, 2)]
+
 # TT only needs a large, a small and a scalar-load tile.
 TT_TILES = [(128, 128, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 4, 4, 1), (64, 64, 16, 2, 2, 1, 1, 1)]
 
@@ -188,6 +191,12 @@ def main():
                            % ("gemm_%dx%dx%d_w%dx%d_%s_v44%s_dma%d" % (bm, bn, bk, wm, wn, layout,
                                                                      "_o%d" % occ if occ > 1 else "", st),
                               bm, bn, bk, wm, wn, st, ta, tb, occ))
+        for t in (DMA_STREAMK if layout == "nn" else []):
+            bm, bn, bk, wm, wn, st, occ = t
+            entries.append("PK_GEMM_DMA_SK(%s, %d, %d, %d, %d, %d, %d, %d)"
+                           % ("gemm_%dx%dx%d_w%dx%d_nn_v44%s_dma%d_sk" % (bm, bn, bk, wm, wn,
+                                                                        "_o%d" % occ if occ > 1 else "", st),
+                              bm, bn, bk, wm, wn, st, occ))
         for t in (DEEP if layout == "nn" else []):
             bm, bn, bk, wm, wn, va, vb, occ = t
             entries.append("PK_GEMM_D(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
@@ -215,6 +224,18 @@ def main():
         bm, bn, bk, wm, wn, va, vb, occ = t
         entries.append("PK_CONV_SK(%s, %d, %d, %d, %d, %d, %d, %d, %d)"
                        % (_name("conv", t, streamk=True), bm, bn, bk, wm, wn, va, vb, occ))
+    for t in DMA:
+        bm, bn, bk, wm, wn, st, occ = t
+        if (4 * (64 * wm * wn // 64)) % (bk // 4):
+            continue  # the gather needs one chunk per lane across its copy slots
+        entries.append("PK_CONV_DMA(%s, %d, %d, %d, %d, %d, %d, %d)"
+                       % ("conv_%dx%dx%d_w%dx%d_v44%s_dma%d" % (bm, bn, bk, wm, wn, "_o%d" % occ if occ > 1 else "", st),
+                          bm, bn, bk, wm, wn, st, occ))
+    for t in DMA_STREAMK:
+        bm, bn, bk, wm, wn, st, occ = t
+        entries.append("PK_CONV_DMA_SK(%s, %d, %d, %d, %d, %d, %d, %d)"
+                       % ("conv_%dx%dx%d_w%dx%d_v44%s_dma%d_sk" % (bm, bn, bk, wm, wn, "_o%d" % occ if occ > 1 else "", st),
+                          bm, bn, bk, wm, wn, st, occ))
     _file("pk_inst_conv.hip", "implicit-GEMM convolution instances (A gathered from an NHWC "
           "image, B the HWIO filter viewed as (KH*KW*Cin) x Cout).", "configs_conv", entries)
 

@@ -153,77 +153,113 @@ const TunedShape kTuned[] = {
     {0, 0, 0, 4096, 4096, 4096, 0, 0, "gemm_128x128x32_w2x4_nn_v44_o2_dma2", 0},
     {0, 1, 0, 4096, 4096, 4096, 0, 0, "gemm_128x128x32_w2x4_tn_v44_o2_dma2", 0},
     {0, 0, 1, 4096, 4096, 4096, 0, 0, "gemm_256x256x16_w2x4_nt_v44_o2_dma4", 0},
-    {0, 0, 0, 2048, 2048, 2048, 0, 0, "gemm_64x64x32_w2x2_nn_v44", 0},
-    // VGG-16 block-first layers at batch 32 (3x3, stride 1)
-    {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_p", 1},
-    {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
-    {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
-    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_sk", 1},
-    // ResNet-50 bottleneck layers at batch 32
-    {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},
-    {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x32_w2x4_v44_o2_d2", 1},
-    {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},
-    {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},
-    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 6},
-    {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x64_w2x4_nn_v44_o2", 1},
-    // the other VGG-16 / ResNet-50 layers of the paper's tables at batch 1 and 4
-    // where the automated search (pk_tune_conv2d_fwd, whose candidates include
-    // the rules' own choice) found a faster configuration or split
-    {1, 0, 0, 12544, 128, 576, 3, 1, "conv_64x64x32_w2x2_v44_d2", 1},  // vgg16 conv2_1 b1 112x112x64->128 3x3 s1
-    {1, 0, 0, 12544, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_d2", 1},  // vgg16 conv2_2 b1 112x112x128->128 3x3 s1
-    {1, 0, 0, 3136, 256, 1152, 3, 1, "conv_64x64x32_w2x2_v44_d2", 2},  // vgg16 conv3_1 b1 56x56x128->256 3x3 s1
-    {1, 0, 0, 3136, 256, 2304, 3, 1, "conv_64x64x16_w2x2_v44", 6},  // vgg16 conv3_2 b1 56x56x256->256 3x3 s1
-    {1, 0, 0, 784, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_d2", 9},  // vgg16 conv4_1 b1 28x28x256->512 3x3 s1
-    {1, 0, 0, 784, 512, 4608, 3, 1, "conv_128x128x64_w2x4_v44_o2", 9},  // vgg16 conv4_2 b1 28x28x512->512 3x3 s1
-    {1, 0, 0, 196, 512, 4608, 3, 1, "conv_64x64x64_w2x2_v44", 8},  // vgg16 conv5_1 b1 14x14x512->512 3x3 s1
+    // Every distinct VGG-16 / ResNet-50 layer of the paper's tables at batch 32,
+    // 1 and 4 (the benchmark step's layers among them): the automated
+    // search's choice (pk_tune_conv2d_fwd, whose candidates include the rules'
+    // own choice), one configuration and split per (M, Cout, K, window, stride)
+    {1, 0, 0, 1605632, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b32 224x224x3->64 3x3 s1
+    {1, 0, 0, 1605632, 64, 576, 3, 1, "conv_256x64x16_w4x1_v44", 1},  // vgg16 conv1_2 b32 224x224x64->64 3x3 s1
+    {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // vgg16 conv2_1 b32 112x112x64->128 3x3 s1
+    {1, 0, 0, 401408, 128, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // vgg16 conv2_2 b32 112x112x128->128 3x3 s1
+    {1, 0, 0, 100352, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv3_1 b32 56x56x128->256 3x3 s1
+    {1, 0, 0, 100352, 256, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv3_2 b32 56x56x256->256 3x3 s1
+    {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_1 b32 28x28x256->512 3x3 s1
+    {1, 0, 0, 25088, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_2 b32 28x28x512->512 3x3 s1
+    {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv5_1 b32 14x14x512->512 3x3 s1
+    {1, 0, 0, 401408, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b32 230x230x3->64 7x7 s2
+    {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},  // resnet50 conv2_1 b32 56x56x64->256 1x1 s1
+    {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv2_2 b32 56x56x64->64 1x1 s1 (in the step: the B-resident form is faster alone, slower there)
+    {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // resnet50 conv2_3 b32 56x56x64->64 3x3 s1
+    {1, 0, 0, 100352, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_4 b32 56x56x256->64 1x1 s1
+    {1, 0, 0, 25088, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv2_5 b32 56x56x64->64 3x3 s2
+    {1, 0, 0, 25088, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b32 28x28x64->256 1x1 s1
+    {1, 0, 0, 25088, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_2 b32 28x28x256->512 1x1 s1
+    {1, 0, 0, 25088, 128, 256, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv3_3 b32 28x28x256->128 1x1 s1
+    {1, 0, 0, 25088, 128, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // resnet50 conv3_4 b32 28x28x128->128 3x3 s1
+    {1, 0, 0, 25088, 512, 128, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv3_5 b32 28x28x128->512 1x1 s1
+    {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv3_6 b32 28x28x512->128 1x1 s1
+    {1, 0, 0, 6272, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv3_7 b32 28x28x128->128 3x3 s2
+    {1, 0, 0, 6272, 512, 128, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv4_1 b32 14x14x128->512 1x1 s1
+    {1, 0, 0, 6272, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_2 b32 14x14x512->1024 1x1 s1
+    {1, 0, 0, 6272, 256, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_3 b32 14x14x512->256 1x1 s1
+    {1, 0, 0, 6272, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 3},  // resnet50 conv4_4 b32 14x14x256->256 3x3 s1
+    {1, 0, 0, 6272, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 1},  // resnet50 conv4_5 b32 14x14x256->1024 1x1 s1
+    {1, 0, 0, 6272, 256, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_6 b32 14x14x1024->256 1x1 s1
+    {1, 0, 0, 1568, 256, 2304, 3, 2, "conv_128x128x32_w2x4_v44_o2_dma2", 9},  // resnet50 conv4_7 b32 14x14x256->256 3x3 s2
+    {1, 0, 0, 1568, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv5_1 b32 7x7x256->1024 1x1 s1
+    {1, 0, 0, 1568, 2048, 1024, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_2 b32 7x7x1024->2048 1x1 s1
+    {1, 0, 0, 1568, 512, 1024, 1, 1, "gemm_64x64x32_w2x2_k4_nn_v44_d2", 1},  // resnet50 conv5_3 b32 7x7x1024->512 1x1 s1
+    {1, 0, 0, 1568, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv5_4 b32 7x7x512->512 3x3 s1
+    {1, 0, 0, 1568, 2048, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_5 b32 7x7x512->2048 1x1 s1
+    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 6},  // resnet50 conv5_6 b32 7x7x2048->512 1x1 s1
+    {1, 0, 0, 50176, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b1 224x224x3->64 3x3 s1
+    {1, 0, 0, 50176, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // vgg16 conv1_2 b1 224x224x64->64 3x3 s1
+    {1, 0, 0, 12544, 128, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv2_1 b1 112x112x64->128 3x3 s1
+    {1, 0, 0, 12544, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv2_2 b1 112x112x128->128 3x3 s1
+    {1, 0, 0, 3136, 256, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv3_1 b1 56x56x128->256 3x3 s1
+    {1, 0, 0, 3136, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // vgg16 conv3_2 b1 56x56x256->256 3x3 s1
+    {1, 0, 0, 784, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 9},  // vgg16 conv4_1 b1 28x28x256->512 3x3 s1
+    {1, 0, 0, 784, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 12},  // vgg16 conv4_2 b1 28x28x512->512 3x3 s1
+    {1, 0, 0, 196, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 8},  // vgg16 conv5_1 b1 14x14x512->512 3x3 s1
+    {1, 0, 0, 200704, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b4 224x224x3->64 3x3 s1
+    {1, 0, 0, 200704, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv1_2 b4 224x224x64->64 3x3 s1
+    {1, 0, 0, 50176, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // vgg16 conv2_1 b4 112x112x64->128 3x3 s1
+    {1, 0, 0, 50176, 128, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv2_2 b4 112x112x128->128 3x3 s1
+    {1, 0, 0, 12544, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // vgg16 conv3_1 b4 56x56x128->256 3x3 s1
+    {1, 0, 0, 12544, 256, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv3_2 b4 56x56x256->256 3x3 s1
+    {1, 0, 0, 3136, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 3},  // vgg16 conv4_1 b4 28x28x256->512 3x3 s1
+    {1, 0, 0, 3136, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_2 b4 28x28x512->512 3x3 s1
+    {1, 0, 0, 12544, 64, 147, 7, 2, "conv_64x64x16_w2x2_v11", 1},  // resnet50 conv1_1 b1 230x230x3->64 7x7 s2
     {1, 0, 0, 3136, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b1 56x56x64->256 1x1 s1
-    {1, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
-    {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x64_w2x2_v44", 8},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
-    {1, 0, 0, 3136, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_d2", 6},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
-    {1, 0, 0, 784, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44", 8},  // resnet50 conv2_5 b1 56x56x64->64 3x3 s2
+    {1, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
+    {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 3},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
+    {1, 0, 0, 3136, 64, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
+    {1, 0, 0, 784, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 8},  // resnet50 conv2_5 b1 56x56x64->64 3x3 s2
     {1, 0, 0, 784, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b1 28x28x64->256 1x1 s1
-    {1, 0, 0, 784, 512, 256, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
-    {1, 0, 0, 784, 128, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 6},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
-    {1, 0, 0, 784, 128, 1152, 3, 1, "conv_64x64x16_w2x2_v44", 9},  // resnet50 conv3_4 b1 28x28x128->128 3x3 s1
-    {1, 0, 0, 784, 512, 128, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 1},  // resnet50 conv3_5 b1 28x28x128->512 1x1 s1
-    {1, 0, 0, 784, 128, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 6},  // resnet50 conv3_6 b1 28x28x512->128 1x1 s1
-    {1, 0, 0, 196, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44", 16},  // resnet50 conv3_7 b1 28x28x128->128 3x3 s2
-    {1, 0, 0, 196, 512, 128, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 1},  // resnet50 conv4_1 b1 14x14x128->512 1x1 s1
-    {1, 0, 0, 196, 1024, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 6},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
-    {1, 0, 0, 196, 256, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 8},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
-    {1, 0, 0, 196, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44", 12},  // resnet50 conv4_4 b1 14x14x256->256 3x3 s1
-    {1, 0, 0, 196, 1024, 256, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 8},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
-    {1, 0, 0, 196, 256, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 12},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
-    {1, 0, 0, 49, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44", 16},  // resnet50 conv4_7 b1 14x14x256->256 3x3 s2
-    {1, 0, 0, 49, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 4},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
-    {1, 0, 0, 49, 2048, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 12},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
-    {1, 0, 0, 49, 512, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 12},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
-    {1, 0, 0, 49, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44", 16},  // resnet50 conv5_4 b1 7x7x512->512 3x3 s1
-    {1, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
-    {1, 0, 0, 49, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 16},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
-    {1, 0, 0, 50176, 128, 1152, 3, 1, "conv_128x128x16_w2x4_v44_o2_p", 3},  // vgg16 conv2_2 b4 112x112x128->128 3x3 s1
-    {1, 0, 0, 12544, 256, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_d2", 1},  // vgg16 conv3_1 b4 56x56x128->256 3x3 s1
-    {1, 0, 0, 12544, 256, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2", 6},  // vgg16 conv3_2 b4 56x56x256->256 3x3 s1
-    {1, 0, 0, 3136, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44_d2", 3},  // vgg16 conv4_1 b4 28x28x256->512 3x3 s1
-    {1, 0, 0, 3136, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2", 11},  // vgg16 conv4_2 b4 28x28x512->512 3x3 s1
+    {1, 0, 0, 784, 512, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
+    {1, 0, 0, 784, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
+    {1, 0, 0, 784, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv3_4 b1 28x28x128->128 3x3 s1
+    {1, 0, 0, 784, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv3_5 b1 28x28x128->512 1x1 s1
+    {1, 0, 0, 784, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv3_6 b1 28x28x512->128 1x1 s1
+    {1, 0, 0, 196, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv3_7 b1 28x28x128->128 3x3 s2
+    {1, 0, 0, 196, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv4_1 b1 14x14x128->512 1x1 s1
+    {1, 0, 0, 196, 1024, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
+    {1, 0, 0, 196, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
+    {1, 0, 0, 196, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 12},  // resnet50 conv4_4 b1 14x14x256->256 3x3 s1
+    {1, 0, 0, 196, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
+    {1, 0, 0, 196, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 4},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
+    {1, 0, 0, 49, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv4_7 b1 14x14x256->256 3x3 s2
+    {1, 0, 0, 49, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
+    {1, 0, 0, 49, 2048, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 8},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
+    {1, 0, 0, 49, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 8},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
+    {1, 0, 0, 49, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv5_4 b1 7x7x512->512 3x3 s1
+    {1, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
+    {1, 0, 0, 49, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 8},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
     {1, 0, 0, 50176, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b4 230x230x3->64 7x7 s2
     {1, 0, 0, 12544, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b4 56x56x64->256 1x1 s1
-    {1, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
-    {1, 0, 0, 12544, 64, 576, 3, 1, "conv_64x64x64_w2x2_v44", 1},  // resnet50 conv2_3 b4 56x56x64->64 3x3 s1
-    {1, 0, 0, 3136, 64, 576, 3, 2, "conv_64x64x64_w2x2_v44", 8},  // resnet50 conv2_5 b4 56x56x64->64 3x3 s2
-    {1, 0, 0, 3136, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_d2", 1},  // resnet50 conv3_2 b4 28x28x256->512 1x1 s1
-    {1, 0, 0, 3136, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44", 4},  // resnet50 conv3_4 b4 28x28x128->128 3x3 s1
-    {1, 0, 0, 3136, 512, 128, 1, 1, "gemm_64x64x32_w2x2_nn_v44_d2", 1},  // resnet50 conv3_5 b4 28x28x128->512 1x1 s1
-    {1, 0, 0, 3136, 128, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 2},  // resnet50 conv3_6 b4 28x28x512->128 1x1 s1
-    {1, 0, 0, 784, 128, 1152, 3, 2, "conv_64x64x16_w2x2_v44", 9},  // resnet50 conv3_7 b4 28x28x128->128 3x3 s2
-    {1, 0, 0, 784, 256, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 4},  // resnet50 conv4_3 b4 14x14x512->256 1x1 s1
-    {1, 0, 0, 784, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_d2", 9},  // resnet50 conv4_4 b4 14x14x256->256 3x3 s1
-    {1, 0, 0, 784, 256, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 4},  // resnet50 conv4_6 b4 14x14x1024->256 1x1 s1
-    {1, 0, 0, 196, 256, 2304, 3, 2, "conv_64x64x64_w2x2_v44", 16},  // resnet50 conv4_7 b4 14x14x256->256 3x3 s2
-    {1, 0, 0, 196, 2048, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 4},  // resnet50 conv5_2 b4 7x7x1024->2048 1x1 s1
-    {1, 0, 0, 196, 512, 1024, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 8},  // resnet50 conv5_3 b4 7x7x1024->512 1x1 s1
-    {1, 0, 0, 196, 2048, 512, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 6},  // resnet50 conv5_5 b4 7x7x512->2048 1x1 s1
-    {1, 0, 0, 196, 512, 2048, 1, 1, "gemm_64x64x64_w2x2_nn_v44", 8},  // resnet50 conv5_6 b4 7x7x2048->512 1x1 s1
+    {1, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
+    {1, 0, 0, 12544, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv2_3 b4 56x56x64->64 3x3 s1
+    {1, 0, 0, 12544, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_4 b4 56x56x256->64 1x1 s1
+    {1, 0, 0, 3136, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 3},  // resnet50 conv2_5 b4 56x56x64->64 3x3 s2
+    {1, 0, 0, 3136, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_2 b4 28x28x256->512 1x1 s1
+    {1, 0, 0, 3136, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_3 b4 28x28x256->128 1x1 s1
+    {1, 0, 0, 3136, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 4},  // resnet50 conv3_4 b4 28x28x128->128 3x3 s1
+    {1, 0, 0, 3136, 512, 128, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_5 b4 28x28x128->512 1x1 s1
+    {1, 0, 0, 3136, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_6 b4 28x28x512->128 1x1 s1
+    {1, 0, 0, 784, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv3_7 b4 28x28x128->128 3x3 s2
+    {1, 0, 0, 784, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_2 b4 14x14x512->1024 1x1 s1
+    {1, 0, 0, 784, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv4_3 b4 14x14x512->256 1x1 s1
+    {1, 0, 0, 784, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 9},  // resnet50 conv4_4 b4 14x14x256->256 3x3 s1
+    {1, 0, 0, 784, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_5 b4 14x14x256->1024 1x1 s1
+    {1, 0, 0, 784, 256, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 4},  // resnet50 conv4_6 b4 14x14x1024->256 1x1 s1
+    {1, 0, 0, 196, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 12},  // resnet50 conv4_7 b4 14x14x256->256 3x3 s2
+    {1, 0, 0, 196, 2048, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 4},  // resnet50 conv5_2 b4 7x7x1024->2048 1x1 s1
+    {1, 0, 0, 196, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 4},  // resnet50 conv5_3 b4 7x7x1024->512 1x1 s1
+    {1, 0, 0, 196, 2048, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv5_5 b4 7x7x512->2048 1x1 s1
+    {1, 0, 0, 196, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 4},  // resnet50 conv5_6 b4 7x7x2048->512 1x1 s1
+    // ResNet-50 56x56x256 1x1 stride 2 -> 128 at batch 32 (the benchmark step's
+    // reading of that layer; not a row of the paper's table)
+    {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x32_w2x4_v44_o2_dma3", 1},
 };
 
 // Entries recorded at run time by pk_tune_sgemm / pk_tune_conv2d_fwd; they
@@ -295,9 +331,6 @@ bool dma_fits(const Config *c, int64_t lda, int64_t ldb)
 }
 
 // Shapes outside the table, from the same measurements:
-//   - products with at least 4 work-groups of 128 x 128 per CU and K >= 512:
-//     256 x 256 tiles on 8 waves (128 x 64 per wave, 2 waves per SIMD): the
-//     fewest LDS reads and the least L2 traffic per MFMA;
 //   - K <= 64: 64 x 64 tiles; for NN products with K == 64 and N a multiple
 //     of 64, the B-resident form (the whole reduction is one K-block);
 //   - longer reductions with at most one 32 x 64 tile per CU: the reduction
@@ -306,21 +339,34 @@ bool dma_fits(const Config *c, int64_t lda, int64_t ldb)
 //     with at most one 64 x 64 tile per CU, 2 groups of 4 waves on 64 x 64
 //     tiles (the 64 .. 1024 sweep of M, N, K at K >= 128: 1.3-1.8x over
 //     one group, every shape);
-//   - everything larger: 64 x 64 tiles, which keep 4+ waves per SIMD busy;
-//     K-blocks of 32;
+//   - products whose 128 x 128 tiles fill the CUs: 128 x 128 x 32 on 8
+//     waves with both operands copied straight into two LDS stages (at
+//     4096^3 137-139 TFLOP/s for NN and TN, 1.05x the register-staged
+//     256 x 256 tile; 2048^3 1.05x);
+//   - everything between: 64 x 64 x 32 copied straight into three LDS
+//     stages (1.04-1.10x the register-staged 64 x 64 x 32 from 1024^2 x 256
+//     to 4096^3 and on ResNet-50's 1x1 layers);
+//   - the direct-to-LDS forms only where a tile's rows span less than 2 GiB
+//     (else their register-staged twins); TT: register-staged tiles;
 //   - unaligned operands: 4-byte loads.
-const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t ldc, bool vec_ok)
+const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,
+                          bool vec_ok)
 {
     static const char *layout[2][2] = {{"nn", "nt"}, {"tn", "tt"}};
     const char *lay = layout[ta][tb];
     char name[64];
+    auto pick = [&](const char *dma_fmt, const char *reg_fmt) {
+        snprintf(name, sizeof(name), dma_fmt, lay);
+        const Config *c = find_config(name);
+        if (c && dma_fits(c, lda, ldb)) return c;
+        snprintf(name, sizeof(name), reg_fmt, lay);
+        return find_config(name);
+    };
     if (!vec_ok) {
         snprintf(name, sizeof(name), "gemm_64x64x16_w2x2_%s_v11", lay);
     } else if (ta && tb) {
         const bool big = ceil_div(M, 128) * ceil_div(N, 128) >= 4 * kCUs;
         snprintf(name, sizeof(name), big ? "gemm_128x128x16_w2x2_%s_v44" : "gemm_64x64x16_w2x2_%s_v44", lay);
-    } else if (ceil_div(M, 128) * ceil_div(N, 128) >= 4 * kCUs && K >= 512) {
-        snprintf(name, sizeof(name), "gemm_256x256x32_w2x4_%s_v44_o2", lay);
     } else if (K <= 64) {
         snprintf(name, sizeof(name), "gemm_64x64x64_w2x2_%s_v44_br", lay);
         const Config *c = !ta && !tb ? find_config(name) : nullptr;
@@ -330,8 +376,10 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64
         snprintf(name, sizeof(name), "gemm_32x64x32_w1x2_k4_%s_v44_d2", lay);
     } else if (ceil_div(M, 64) * ceil_div(N, 64) <= kCUs) {
         snprintf(name, sizeof(name), "gemm_64x64x32_w2x2_k2_%s_v44_d2", lay);
+    } else if (ceil_div(M, 128) * ceil_div(N, 128) >= kCUs) {
+        return pick("gemm_128x128x32_w2x4_%s_v44_o2_dma2", "gemm_256x256x32_w2x4_%s_v44_o2");
     } else {
-        snprintf(name, sizeof(name), "gemm_64x64x32_w2x2_%s_v44", lay);
+        return pick("gemm_64x64x32_w2x2_%s_v44_dma3", "gemm_64x64x32_w2x2_%s_v44");
     }
     return find_config(name);
 }
@@ -345,18 +393,27 @@ bool conv_config_fits(const Config *c, bool va4, bool vb4)
     return true;
 }
 
-// Convolutions: 64 x 64 x 32 was the fastest or within 1% of it on every
-// VGG-16 / ResNet-50 layer with Cin % 4 == 0; channel counts that break
-// 16-byte alignment use 4-byte gathers.
-const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4)
+// Convolutions with Cin and Cout multiples of 4 (16-byte gathers):
+//   - Cout >= 128 and 128 x 128 tiles filling the CUs: 128 x 128 x 32 on 8
+//     waves, both operands copied straight into two LDS stages (VGG-16
+//     conv2_2 / conv3_2 / conv4_2 and ResNet-50 28x28 3x3 at batch 32:
+//     1.10-1.19x the register-staged 64 x 64 x 32);
+//   - other Cout >= 128: 64 x 64 x 32 copied straight into three stages;
+//   - Cout < 128: the register-staged 64 x 64 x 32 (ResNet-50 56x56x64 3x3:
+//     the fastest measured);
+//   - the direct-to-LDS forms only while the image spans less than 2 GiB.
+// Channel counts that break 16-byte alignment use 4-byte gathers.
+const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4, bool dma_ok)
 {
-    (void)M;
-    (void)Cout;
     const char *name;
-    if (va4 && vb4)
-        name = "conv_64x64x32_w2x2_v44";
-    else
+    if (!(va4 && vb4))
         name = "conv_64x64x16_w2x2_v11";
+    else if (!dma_ok || Cout < 128)
+        name = "conv_64x64x32_w2x2_v44";
+    else if (ceil_div(M, 128) * ceil_div(Cout, 128) >= kCUs)
+        name = "conv_128x128x32_w2x4_v44_o2_dma2";
+    else
+        name = "conv_64x64x32_w2x2_v44_dma3";
     return find_config(name);
 }
 
@@ -663,7 +720,7 @@ int pk_sgemm_ws(char transA, char transB, int64_t M, int64_t N, int64_t K, float
                   (c->streamk && !streamk_ok(c))))
             c = nullptr;
         if (c) splits = t->splits;
-        if (!c) c = select_gemm(ta, tb, M, N, K, ldc, vec_ok);
+        if (!c) c = select_gemm(ta, tb, M, N, K, lda, ldb, ldc, vec_ok);
         if (!c) return PK_ERR_NOT_SUPPORTED;
     }
     (void)was_forced;
@@ -736,7 +793,7 @@ size_t pk_sgemm_workspace_bytes(char transA, char transB, int64_t M, int64_t N, 
         }
         if (c && !gemm_config_fits(c, ta, tb, vec_ok)) c = nullptr;
         if (!c) {
-            c = select_gemm(ta, tb, M, N, K, N, vec_ok);
+            c = select_gemm(ta, tb, M, N, K, ta ? M : K, tb ? K : N, N, vec_ok);
             splits = 0;
         }
     }
@@ -778,7 +835,10 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
         const bool direct_ok = !gemm_path && pk::direct_conv_fits(nullptr, W, Wo, Cout, KH, KW, Cin, sh, sw) && N <= 65535;
         if (direct_ok && !(tuned && v4)) return 0;
         c = (tuned && v4) ? find_config(tuned->config) : nullptr;
-        if (!c) c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cout, v4) : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0);
+        if (!c)
+            c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cin, Cout, Cout, v4)
+                          : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0,
+                                        (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31));
     }
     if (!c || c->kind == pk::KIND_DIRECT) return 0;
     if (c->streamk) {
@@ -869,7 +929,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         } else {
             c = (tuned && vec_ok) ? find_config(tuned->config) : nullptr;
             if (c && (!bres_fits(c, Cout, Cin, Cout) || !dma_fits(c, Cin, Cout))) c = nullptr;
-            if (!c) c = select_gemm(0, 0, M, Cout, Cin, Cout, vec_ok);
+            if (!c) c = select_gemm(0, 0, M, Cout, Cin, Cin, Cout, Cout, vec_ok);
             // a forced split needs a form that splits K across work-groups
             if (c && t_forced_splits > 1 && c->bres)
                 c = find_config(vec_ok ? "gemm_64x64x32_w2x2_nn_v44" : "gemm_64x64x16_w2x2_nn_v11");
@@ -879,15 +939,19 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         auto direct_ok = [&](const Config *d) {
             return N <= 65535 && pk::direct_conv_fits(d, W, Wo, Cout, KH, KW, Cin, sh, sw);
         };
+        // the direct-to-LDS gather addresses the image in 32-bit byte offsets
+        const bool dma_ok = (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31);
         if (c) {
-            if (!conv_config_fits(c, va4, vb4)) return PK_ERR_NOT_SUPPORTED;
+            if (!conv_config_fits(c, va4, vb4) || (c->dma && !dma_ok)) return PK_ERR_NOT_SUPPORTED;
             if (c->kind == pk::KIND_DIRECT && !direct_ok(c)) return PK_ERR_NOT_SUPPORTED;
         } else {
             // a measured choice first (it may name the direct kernel), then the
             // rules: the persistent direct form when its patch fits, else the
             // one-tile-per-work-group form
             c = tuned ? find_config(tuned->config) : nullptr;
-            if (c && (!conv_config_fits(c, va4, vb4) || (c->kind == pk::KIND_DIRECT && !direct_ok(c)))) c = nullptr;
+            if (c && (!conv_config_fits(c, va4, vb4) || (c->kind == pk::KIND_DIRECT && !direct_ok(c)) ||
+                      (c->dma && !dma_ok)))
+                c = nullptr;
             if (!c) {
                 for (const char *name : {"direct_8x32x64_k32_p", "direct_8x32x64_k32"}) {
                     const Config *d = find_config(name);
@@ -897,7 +961,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
                     }
                 }
             }
-            if (!c) c = select_conv(M, Cout, va4, vb4);
+            if (!c) c = select_conv(M, Cout, va4, vb4, dma_ok);
         }
         if (!c) return PK_ERR_NOT_SUPPORTED;
         a.H = (int)H;
@@ -924,7 +988,8 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         } else if (was_forced) {
             return planned ? PK_ERR_WORKSPACE : PK_ERR_NOT_SUPPORTED;
         } else {
-            c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cout, vec_ok) : select_conv(M, Cout, va4, vb4);
+            c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cin, Cout, Cout, vec_ok)
+                          : select_conv(M, Cout, va4, vb4, (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31));
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     }
@@ -1016,7 +1081,11 @@ const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok
     (void)Cout;
     const Config *c = forced(bad);
     if (*bad) return nullptr;
-    if (c) return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent && !c->streamk && !c->bres && !c->dma) ? c : nullptr;
+    // the 16 products are (T x Cin) (Cin x Cout), lda = Cin, ldb = Cout
+    if (c)
+        return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent && !c->streamk && !c->bres && dma_fits(c, Cin, Cout))
+                   ? c
+                   : nullptr;
     if (!vec_ok) return find_config("gemm_64x64x16_w2x2_nn_v11");
     return find_config(Cin <= 128 ? "gemm_64x64x16_w2x2_nn_v44" : "gemm_64x64x32_w2x2_nn_v44");
 }

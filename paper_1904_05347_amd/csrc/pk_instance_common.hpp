@@ -99,6 +99,45 @@ static hipError_t launch_gemm_streamk(const KernelArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int AMODE, bool TB, int OCC>
+static int resident_dma_streamk(int beta)
+{
+    static int per_cu[2] = {0, 0};  // the same on every MI355X
+    const int b = beta ? 1 : 0;
+    if (per_cu[b] == 0) {
+        auto kernel = gemm_dma_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, AMODE, TB, OCC, false>;
+        if constexpr (AMODE != A_CONV) {
+            if (b) kernel = gemm_dma_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, AMODE, TB, OCC, true>;
+        }
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, 64 * WAVES_M * WAVES_N, 0) != hipSuccess ||
+            n < 1)
+            n = 1;
+        per_cu[b] = n;
+    }
+    return per_cu[b];
+}
+
+// Stream-K launch of the direct-to-LDS contraction (as launch_gemm_streamk).
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int AMODE, bool TB, int OCC>
+static hipError_t launch_gemm_dma_streamk(const KernelArgs &a, hipStream_t stream)
+{
+    if (a.sk_groups < 1 || !a.sk_part || !a.sk_cnt || a.sk_nkb < 1) return hipErrorInvalidValue;
+    const hipError_t z = launch_zero_ints(a.sk_cnt, a.tiles_m * a.tiles_n, stream);
+    if (z != hipSuccess) return z;
+    const dim3 grid((unsigned)a.sk_groups), block(64 * WAVES_M * WAVES_N);
+    if constexpr (AMODE != A_CONV) {
+        if (reads_c<AMODE>(a)) {
+            hipLaunchKernelGGL((gemm_dma_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, AMODE, TB, OCC, true>),
+                               grid, block, 0, stream, a);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((gemm_dma_streamk_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, AMODE, TB, OCC, false>), grid,
+                       block, 0, stream, a);
+    return hipGetLastError();
+}
+
 // B-resident streaming launch: as many work-groups as the CUs hold, a
 // multiple of (XCD count) x (column blocks N / BN), each walking a contiguous
 // range of row tiles of one column block.
@@ -149,17 +188,19 @@ static hipError_t launch_gemm_ksplit(const KernelArgs &a, hipStream_t stream)
 
 // Direct-to-LDS staging (same grid as launch_gemm; dense operands).  The
 // host checks that the rows one tile addresses span less than 2 GiB.
-template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, bool TA, bool TB, int OCC>
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int AMODE, bool TB, int OCC>
 static hipError_t launch_gemm_dma(const KernelArgs &a, hipStream_t stream)
 {
     const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
     const dim3 block(64 * WAVES_M * WAVES_N);
-    if (reads_c<A_KCONTIG>(a)) {
-        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, TA, TB, OCC, true>), grid, block, 0,
-                           stream, a);
-        return hipGetLastError();
+    if constexpr (AMODE != A_CONV) {
+        if (reads_c<AMODE>(a)) {
+            hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, AMODE, TB, OCC, true>), grid,
+                               block, 0, stream, a);
+            return hipGetLastError();
+        }
     }
-    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, TA, TB, OCC, false>), grid, block, 0,
+    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, BK, WAVES_M, WAVES_N, STAGES, AMODE, TB, OCC, false>), grid, block, 0,
                        stream, a);
     return hipGetLastError();
 }
@@ -239,7 +280,22 @@ static constexpr int lds_bytes()
 
 #define PK_GEMM_DMA(name, BM, BN, BK, WM, WN, STAGES, TA, TB, OCC)                                    \
     {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, 4, 4, OCC, 0, STAGES * 4 * (BM * BK + BK * BN),     \
-     &launch_gemm_dma<BM, BN, BK, WM, WN, STAGES, (TA != 0), (TB != 0), OCC>, 0, 0, nullptr, 0, 1, STAGES}
+     &launch_gemm_dma<BM, BN, BK, WM, WN, STAGES, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), OCC>, 0, 0, nullptr, 0, 1, \
+     STAGES}
+
+#define PK_CONV_DMA(name, BM, BN, BK, WM, WN, STAGES, OCC)                                           \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, 4, 4, OCC, 0, STAGES * 4 * (BM * BK + BK * BN),      \
+     &launch_gemm_dma<BM, BN, BK, WM, WN, STAGES, A_CONV, false, OCC>, 0, 0, nullptr, 0, 1, STAGES}
+
+#define PK_GEMM_DMA_SK(name, BM, BN, BK, WM, WN, STAGES, OCC)                                       \
+    {#name, KIND_GEMM, BM, BN, BK, WM, WN, 0, 0, 4, 4, OCC, 0, STAGES * 4 * (BM * BK + BK * BN),       \
+     &launch_gemm_dma_streamk<BM, BN, BK, WM, WN, STAGES, A_KCONTIG, false, OCC>, 0, 1,                \
+     &resident_dma_streamk<BM, BN, BK, WM, WN, STAGES, A_KCONTIG, false, OCC>, 0, 1, STAGES}
+
+#define PK_CONV_DMA_SK(name, BM, BN, BK, WM, WN, STAGES, OCC)                                        \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, 4, 4, OCC, 0, STAGES * 4 * (BM * BK + BK * BN),       \
+     &launch_gemm_dma_streamk<BM, BN, BK, WM, WN, STAGES, A_CONV, false, OCC>, 0, 1,                   \
+     &resident_dma_streamk<BM, BN, BK, WM, WN, STAGES, A_CONV, false, OCC>, 0, 1, STAGES}
 
 #define PK_CONV_D(name, BM, BN, BK, WM, WN, VA, VB, OCC)                                               \
     {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, VA, VB, OCC, 0,                                      \

@@ -653,20 +653,92 @@ struct DmaOperand {
     }
 };
 
-// The contraction (dense operands, any of the four layouts) with both
-// operand tiles copied straight into STAGES LDS stages (DmaOperand): S-1
+// The implicit-GEMM gather of A (NHWC image, Cin % 4 == 0) copied straight
+// into LDS in DmaOperand's KROWS layout: row m of the tile is output pixel
+// (n, ho, wo), chunk c its taps' channels 4c .. 4c+3 of the current
+// K-block.  With 4 * NW a multiple of CPR every copy slot of a lane has the
+// same chunk c, so one (kh, kw, ci) walk per lane serves all of them.  Taps
+// outside the image, rows past M and k past K read as zero (offset past the
+// buffer's range); offsets count from the image base, so the host checks
+// that the input spans less than 2 GiB.
+template <int BM, int BK, int NW>
+struct DmaConvA {
+    typedef DmaOperand<BM, BK, NW, true> Layout;
+    static constexpr int CPR = Layout::CPR, RPS = Layout::RPS, L = Layout::L, FLOATS = Layout::FLOATS;
+    static_assert((4 * NW) % CPR == 0, "one chunk per lane across the copy slots");
+    int nb[L], ih0[L], iw0[L];  // image row base n*H and window origin of each slot's pixel
+    int col;                    // this lane's k offset inside the K-block
+    int ci, kw, kh;             // decomposition of the lane's current k
+    int H, W, Cin, KW;
+
+    __device__ __forceinline__ void init(const KernelArgs &p, int m0, int kbeg, int wave, int lane)
+    {
+        H = p.H; W = p.W; Cin = p.Cin; KW = p.KW;
+        const int r_first = ((wave * 64) + lane) / CPR;
+        col = 4 * ((lane % CPR) ^ ((r_first / RPS) % CPR));
+#pragma unroll
+        for (int i = 0; i < L; ++i) {
+            const int m = m0 + ((i * NW + wave) * 64 + lane) / CPR;
+            if (m < p.M) {
+                const int wo = m % p.Wo;
+                const int t = m / p.Wo;
+                const int ho = t % p.Ho;
+                nb[i] = (t / p.Ho) * H;
+                ih0[i] = ho * p.sh - p.pt;
+                iw0[i] = wo * p.sw - p.pl;
+            } else {
+                nb[i] = 0;
+                ih0[i] = -(1 << 28);  // every tap falls outside the image
+                iw0[i] = 0;
+            }
+        }
+        const int k = kbeg * BK + col;
+        const int tap = k / Cin;
+        ci = k - tap * Cin;
+        kh = tap / KW;
+        kw = tap - kh * KW;
+    }
+    // copy K-block k0 (the one the walk stands at) into `tile`, then step the walk
+    __device__ __forceinline__ void issue(const float *x, int k0, int K, float *tile, int wave)
+    {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)x, 0, 0x7fffffff, 0x00020000);
+        const bool k_ok = k0 + col < K;
+#pragma unroll
+        for (int i = 0; i < L; ++i) {
+            const int ih = ih0[i] + kh, iw = iw0[i] + kw;
+            const bool ok = k_ok && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
+            const int o = ok ? (((nb[i] + ih) * W + iw) * Cin + ci) * 4 : (int)0x80000000;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs, (__attribute__((address_space(3))) void *)(tile + (i * NW + wave) * 256), 16, o, 0, 0, 0);
+        }
+        ci += BK;
+        while (ci >= Cin) {
+            ci -= Cin;
+            if (++kw == KW) { kw = 0; ++kh; }
+        }
+    }
+    __device__ __forceinline__ static void read4(const float *tile, int row, int h, int g, float *v)
+    {
+        Layout::read4(tile, row, h, g, v);
+    }
+};
+
+// The contraction (dense operands in any of the four layouts, or the
+// convolution's implicit-GEMM gather) with both operand tiles copied
+// straight into STAGES LDS stages (DmaOperand, DmaConvA): S-1
 // K-blocks are in flight at no register cost.  The compiler does not see
 // these writes to LDS, so every wait for them is explicit and followed by a
 // compiler memory barrier, and the work-group barrier is issued without
 // __syncthreads()'s fence (which would also wait for the copies in flight
 // for later blocks).  Same MFMA group pipeline as gemm_kernel.
-template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, bool TA, bool TB, int OCC, bool BETA>
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int AMODE, bool TB, int OCC, bool BETA>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 gemm_dma_kernel(KernelArgs p)
 {
     typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, false, 4, 4> G;  // MFMA and epilogue only
     constexpr int NW = G::NT / 64;
-    typedef DmaOperand<BM, BK, NW, !TA> OpA;
+    typedef typename std::conditional<AMODE == A_CONV, DmaConvA<BM, BK, NW>,
+                                      DmaOperand<BM, BK, NW, AMODE == A_KCONTIG>>::type OpA;
     typedef DmaOperand<BN, BK, NW, TB> OpB;
     constexpr int A_ST = OpA::FLOATS, B_ST = OpB::FLOATS;  // floats per stage
     constexpr int LPB = OpA::L + OpB::L;                    // copies per lane per K-block
@@ -681,7 +753,7 @@ gemm_dma_kernel(KernelArgs p)
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int l32 = lane & 31, h = lane >> 5;
 
-    {  // product blockIdx.y of a batch
+    if constexpr (AMODE != A_CONV) {  // product blockIdx.y of a batch
         const int64_t bz = blockIdx.y;
         p.A += bz * p.stride_a;
         p.B += bz * p.stride_b;
@@ -695,11 +767,18 @@ gemm_dma_kernel(KernelArgs p)
 
     OpA oa;
     OpB ob;
-    oa.init(p.lda, m0, p.M, wave, lane);
+    if constexpr (AMODE == A_CONV)
+        oa.init(p, m0, kbeg, wave, lane);
+    else
+        oa.init(p.lda, m0, p.M, wave, lane);
     ob.init(p.ldb, n0, p.N, wave, lane);
+    // blocks are issued in K order (the gather's walk steps once per issue)
     auto issue = [&](int kb, int s) {
         float *as = smem + s * (A_ST + B_ST);
-        oa.issue(p.A, p.lda, m0, kb * BK, p.K, as, wave);
+        if constexpr (AMODE == A_CONV)
+            oa.issue(p.A, kb * BK, p.K, as, wave);
+        else
+            oa.issue(p.A, p.lda, m0, kb * BK, p.K, as, wave);
         ob.issue(p.B, p.ldb, n0, kb * BK, p.K, as + A_ST, wave);
     };
     // wait until this lane's copies of every issued block but the newest
@@ -1456,6 +1535,194 @@ gemm_streamk_kernel(KernelArgs p)
     }
 }
 
+
+// Stream-K form of the direct-to-LDS contraction: the grid is the resident
+// work-groups and each walks its share of the (tile, K-block) iterations as
+// gemm_streamk_kernel does, with the copies issued STAGES-1 iterations ahead
+// across tile boundaries (the operand helpers are set up again whenever the
+// copies enter a new tile; the LDS stage ring runs on unbroken).  Partial
+// tiles are published and finished by their last contributor in K order, as
+// there.  The epilogue's stores count on the same vector-memory counter as
+// the copies and retire in order, so a wait issued after them only waits
+// longer, never too little.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int AMODE, bool TB, int OCC, bool BETA>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_dma_streamk_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, false, 4, 4> G;  // MFMA and epilogue only
+    constexpr int NT = G::NT, NW = NT / 64;
+    typedef typename std::conditional<AMODE == A_CONV, DmaConvA<BM, BK, NW>,
+                                      DmaOperand<BM, BK, NW, AMODE == A_KCONTIG>>::type OpA;
+    typedef DmaOperand<BN, BK, NW, TB> OpB;
+    constexpr int A_ST = OpA::FLOATS, B_ST = OpB::FLOATS;
+    constexpr int LPB = OpA::L + OpB::L;
+    static_assert(STAGES >= 2 && STAGES <= 4, "two to four LDS stages");
+    static_assert((STAGES - 2) * LPB <= 63, "vmcnt range");
+
+    __shared__ __attribute__((aligned(16))) float smem[STAGES * (A_ST + B_ST)];
+    __shared__ int s_arrival;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+    const int nkb = p.sk_nkb;
+    const StreamK sk{p.tiles_m * p.tiles_n * nkb, (int)gridDim.x, nkb};
+
+    // work-group b runs on XCD b % xcds: give each XCD a contiguous share of
+    // the logical ranges, so the tiles an XCD works on are neighbours
+    int lg = blockIdx.x;
+    if (p.xcds > 1 && sk.G % p.xcds == 0) lg = (blockIdx.x % p.xcds) * (sk.G / p.xcds) + blockIdx.x / p.xcds;
+    const int beg = sk.start(lg), end = sk.start(lg + 1);
+    if (beg >= end) return;  // uniform over the work-group, before any barrier
+
+    auto decode_tile = [&](int t, int &m0_, int &n0_) {
+        int tm, tn;
+        tile_of(p, t, tm, tn);
+        m0_ = tm * BM;
+        n0_ = tn * BN;
+    };
+
+    // producer: the next iteration to copy, its stage, and the tile the
+    // operand helpers are set up for
+    OpA oa;
+    OpB ob;
+    int pj = beg, ps = 0, p_tile = -1, pm0 = 0, pn0 = 0;
+    auto issue_next = [&]() {
+        const int t = pj / nkb, kb = pj - t * nkb;
+        if (t != p_tile) {
+            p_tile = t;
+            decode_tile(t, pm0, pn0);
+            if constexpr (AMODE == A_CONV)
+                oa.init(p, pm0, kb, wave, lane);
+            else
+                oa.init(p.lda, pm0, p.M, wave, lane);
+            ob.init(p.ldb, pn0, p.N, wave, lane);
+        }
+        float *as = smem + ps * (A_ST + B_ST);
+        if constexpr (AMODE == A_CONV)
+            oa.issue(p.A, kb * BK, p.K, as, wave);
+        else
+            oa.issue(p.A, p.lda, pm0, kb * BK, p.K, as, wave);
+        ob.issue(p.B, p.ldb, pn0, kb * BK, p.K, as + A_ST, wave);
+        ++pj;
+        ps = ps + 1 == STAGES ? 0 : ps + 1;
+    };
+    auto wait_blocks = [&](int later) {
+        if (STAGES >= 4 && later >= 2)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPB) : "memory");
+        else if (STAGES >= 3 && later >= 1)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPB) : "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+    auto barrier = [] {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    auto read_group = [&](const float *as, int g, typename G::FragA &xa, typename G::FragB &xb) {
+#pragma unroll
+        for (int i = 0; i < G::RM; ++i) OpA::read4(as, a_row + i * 32, h, g, xa[i]);
+#pragma unroll
+        for (int j = 0; j < G::RN; ++j) OpB::read4(as + A_ST, b_row + j * 32, h, g, xb[j]);
+    };
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NGR = G::NG;
+
+    for (int i = 0; i < STAGES - 1 && pj < end; ++i) issue_next();
+    int cj = beg, cs = 0;  // consumer: the iteration being multiplied and its stage
+    wait_blocks(min(STAGES - 2, pj - cj - 1));
+    barrier();
+    read_group(smem, 0, fa[0], fb[0]);
+
+    int tile = beg / nkb;
+    int kbeg = beg - tile * nkb;
+    int m0, n0;
+    decode_tile(tile, m0, n0);
+    for (;;) {
+        if (pj < end) issue_next();
+        const float *as = smem + cs * (A_ST + B_ST);
+#pragma unroll
+        for (int g = 0; g < NGR - 1; ++g) {
+            read_group(as, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        const int cs_next = cs + 1 == STAGES ? 0 : cs + 1;
+        wait_blocks(min(STAGES - 2, pj - cj - 2));
+        barrier();
+        // unconditional (stale after the last iteration, never used)
+        read_group(smem + cs_next * (A_ST + B_ST), 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NGR - 1) & 1], fb[(NGR - 1) & 1]);
+
+        const int kb = cj - tile * nkb;
+        if (kb == nkb - 1 || cj + 1 == end) {
+            const int kend = kb + 1;
+            const int row_base = m0 + wm * G::WM + 4 * h, col_base = n0 + wn * G::WN + l32;
+            bool write = true;  // this work-group writes the tile's C block
+            if (kbeg != 0 || kend != nkb) {
+                // partial tile: publish this range's sum (layout and coherence
+                // as in gemm_streamk_kernel), then the last contributor adds
+                // all of them in K-block order
+                float *mine = p.sk_part + (int64_t)sk.slot(lg, tile) * (BM * BN) + tid;
+                asm volatile("" : "+v"(mine));
+#pragma unroll
+                for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                    for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r)
+                            __hip_atomic_store(mine + ((i * G::RN + j) * 16 + r) * NT, acc[i][j][r],
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
+                __syncthreads();
+                if (tid == 0)
+                    s_arrival = __hip_atomic_fetch_add(p.sk_cnt + tile, 1, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                __syncthreads();
+                const int lo = sk.owner(tile * nkb), hi = sk.owner(tile * nkb + nkb - 1);
+                write = s_arrival == hi - lo;  // the last contributor: uniform over the work-group
+                if (write) {
+                    auto gather = [&](int g, bool first) {
+                        const float *src = p.sk_part + (int64_t)sk.slot(g, tile) * (BM * BN) + tid;
+                        asm volatile("" : "+v"(src));
+#pragma unroll
+                        for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                            for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                                for (int r = 0; r < 16; ++r) {
+                                    const float v = __hip_atomic_load(src + ((i * G::RN + j) * 16 + r) * NT,
+                                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                    acc[i][j][r] = first ? v : acc[i][j][r] + v;
+                                }
+                    };
+                    gather(lo, true);
+                    for (int g = lo + 1; g <= hi; ++g) gather(g, false);
+                }
+            }
+            if (write) G::template store<BETA>(p, acc, row_base, col_base, 0);
+            G::zero(acc);
+            if (cj + 1 < end) {
+                tile = (cj + 1) / nkb;
+                kbeg = 0;
+                decode_tile(tile, m0, n0);
+            }
+        }
+        if (cj + 1 == end) break;
+        ++cj;
+        cs = cs_next;
+    }
+}
 
 // Contraction with op(B) resident in LDS, for short reductions (the 1x1
 // convolutions of ResNet-50's bottlenecks: K = 64 input channels, N = 64 or

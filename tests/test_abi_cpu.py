@@ -232,9 +232,9 @@ def test_config_space(pk):
         assert c["bm"] % (32 * c["waves_m"]) == 0 and c["bn"] % (32 * c["waves_n"]) == 0
         assert c["bk"] % 8 == 0
         if c["dma"]:  # unpadded, swizzled tiles copied straight into 2 to 4 LDS stages
-            assert c["kind"] == 0 and c["stages"] in (2, 3, 4) and c["vec_a"] == c["vec_b"] == 4
+            assert c["kind"] in (0, 1) and c["stages"] in (2, 3, 4) and c["vec_a"] == c["vec_b"] == 4
             assert c["lds_bytes"] == c["stages"] * 4 * (c["bm"] * c["bk"] + c["bk"] * c["bn"]), c["name"]
-            assert c["name"].endswith("_dma%d" % c["stages"])
+            assert c["name"].endswith("_dma%d" % c["stages"]) or c["name"].endswith("_dma%d_sk" % c["stages"])
             continue
         assert c["stages"] in (1, 2)
         assert c["stages"] == 2 or (c["kind"] == 0 and c["name"].endswith("_s1"))

@@ -187,6 +187,44 @@ def test_direct_persistent_loops_over_tiles(geom):
     assert np.array_equal(out.reshape(-1)[idx].astype(np.float64), ref)
 
 
+DMA_GEOMS = [
+    # N, H, W, Cin, KH, KW, Cout, stride, pads (t, l, b, r)
+    (2, 13, 9, 12, 3, 3, 36, (2, 2), (1, 0, 1, 1)),
+    (3, 10, 10, 64, 1, 1, 68, (2, 2), (0, 0, 0, 0)),
+    (1, 12, 11, 4, 5, 5, 8, (1, 1), (2, 2, 2, 2)),
+    (2, 7, 7, 132, 3, 3, 260, (1, 1), (1, 1, 1, 1)),
+]
+
+
+@pytest.mark.parametrize("geom", DMA_GEOMS, ids=lambda g: "%dx%dx%dx%d_k%d_s%d" % (g[0], g[1], g[2], g[3], g[4], g[7][0]))
+def test_conv_dma_geometries(geom):
+    """The direct-to-LDS gather forms on windows beside the 3x3 stride-1 one:
+    stride 2 with asymmetric padding, a strided 1x1, a 5x5, channel counts
+    that are not multiples of the K-block, and a forced split of the
+    reduction (stream-K forms: their own partition); integer data, so every
+    output must equal the oracle bit for bit."""
+    torch, pk = require_gpu()
+    N, H, W, Cin, KH, KW, Cout, stride, pads = geom
+    rng = np.random.default_rng(H * 31 + Cin)
+    x = wl.integers(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+    f = wl.integers(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
+    ref, _ = oracle.conv2d(x, f, stride, pads)
+    Ho, Wo = ref.shape[1], ref.shape[2]
+    ws = torch.empty(2 * N * Ho * Wo * Cout, dtype=torch.float32, device="cuda")
+    ran = 0
+    for cfg in pk.configs():
+        if cfg["kind"] != 1 or not cfg["dma"]:
+            continue
+        # stream-K forms take no split; the binding sizes their workspace
+        for splits in ((0,) if cfg["streamk"] else (0, 2)):
+            out, used = _run(pk, x, f, stride, pads, workspace=ws if splits else None, force=cfg["name"],
+                             splits=splits)
+            assert used == cfg["name"]
+            assert np.array_equal(out.astype(np.float64), ref), (cfg["name"], splits)
+            ran += 1
+    assert ran >= 8
+
+
 @pytest.mark.parametrize("splits", [2, 3, 5])
 def test_conv_split_k_forced(splits):
     torch, pk = require_gpu()
