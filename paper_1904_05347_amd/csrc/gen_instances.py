@@ -79,7 +79,7 @@ KSPLIT = [(64, 64, 16, 2, 2, 4, 1, 4, 4, 1), (64, 64, 32, 2, 2, 4, 1, 4, 4, 1), 
 # Direct-to-LDS staging ("_dmaS", S LDS stages; NN, TN, NT): the
 # register-staged loader's alternative, beside the same tiles.  (BM, BN, BK, WAVES_M, WAVES_N,
 # stages, OCC)
-DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2, 4, 4, 2),
+DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2, 4, 4, 2), (256, 256, 32, 2, 4, 2, 2),
        (128, 128, 32, 2, 4, 2, 2), (128, 128, 32, 2, 4, 3, 2), (128, 128, 32, 2, 4, 4, 2),
        (128, 128, 16, 2, 2, 3, 1), (128, 128, 16, 2, 2, 4, 1), (64, 64, 32, 2, 2, 3, 1)]
 

@@ -150,9 +150,9 @@ struct TunedShape {
 };
 
 const TunedShape kTuned[] = {
-    {0, 0, 0, 4096, 4096, 4096, 0, 0, "gemm_128x128x32_w2x4_nn_v44_o2_dma2", 0},
-    {0, 1, 0, 4096, 4096, 4096, 0, 0, "gemm_128x128x32_w2x4_tn_v44_o2_dma2", 0},
-    {0, 0, 1, 4096, 4096, 4096, 0, 0, "gemm_256x256x16_w2x4_nt_v44_o2_dma4", 0},
+    {0, 0, 0, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_nn_v44_o2_dma2", 0},
+    {0, 1, 0, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_tn_v44_o2_dma2", 0},
+    {0, 0, 1, 4096, 4096, 4096, 0, 0, "gemm_256x256x32_w2x4_nt_v44_o2_dma2", 0},
     // Every distinct VGG-16 / ResNet-50 layer of the paper's tables at batch 32,
     // 1 and 4 (the benchmark step's layers among them): the automated
     // search's choice (pk_tune_conv2d_fwd, whose candidates include the rules'
@@ -339,10 +339,12 @@ bool dma_fits(const Config *c, int64_t lda, int64_t ldb)
 //     with at most one 64 x 64 tile per CU, 2 groups of 4 waves on 64 x 64
 //     tiles (the 64 .. 1024 sweep of M, N, K at K >= 128: 1.3-1.8x over
 //     one group, every shape);
-//   - products whose 128 x 128 tiles fill the CUs: 128 x 128 x 32 on 8
+//   - products whose 256 x 256 tiles fill the CUs: 256 x 256 x 32 on 8
 //     waves with both operands copied straight into two LDS stages (at
-//     4096^3 137-139 TFLOP/s for NN and TN, 1.05x the register-staged
-//     256 x 256 tile; 2048^3 1.05x);
+//     4096^3 140-143 TFLOP/s in NN, TN and NT: 1.05-1.08x the
+//     register-staged 256 x 256 tiles, and half the fetched bytes of a
+//     128 x 128 tile); whose 128 x 128 tiles fill them: 128 x 128 x 32 the
+//     same way (2048^3: 1.05x);
 //   - everything between: 64 x 64 x 32 copied straight into three LDS
 //     stages (1.04-1.10x the register-staged 64 x 64 x 32 from 1024^2 x 256
 //     to 4096^3 and on ResNet-50's 1x1 layers);
@@ -376,6 +378,8 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64
         snprintf(name, sizeof(name), "gemm_32x64x32_w1x2_k4_%s_v44_d2", lay);
     } else if (ceil_div(M, 64) * ceil_div(N, 64) <= kCUs) {
         snprintf(name, sizeof(name), "gemm_64x64x32_w2x2_k2_%s_v44_d2", lay);
+    } else if (ceil_div(M, 256) * ceil_div(N, 256) >= kCUs) {
+        return pick("gemm_256x256x32_w2x4_%s_v44_o2_dma2", "gemm_256x256x32_w2x4_%s_v44_o2");
     } else if (ceil_div(M, 128) * ceil_div(N, 128) >= kCUs) {
         return pick("gemm_128x128x32_w2x4_%s_v44_o2_dma2", "gemm_256x256x32_w2x4_%s_v44_o2");
     } else {
