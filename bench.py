@@ -437,9 +437,10 @@ def run_ablations(torch, pk, wl):
     """The design choices the paper varies, measured on MI355X: double
     buffering (two LDS stages vs one), load vector width (16/8/4 bytes),
     square vs elongated wave tiles at equal accumulator count, tile size
-    against CU fill, and warm vs cold caches for the layers whose working set
-    fits the 256 MB last-level cache.  Median and min of 50 individually
-    timed calls each."""
+    against CU fill, the operand loader (register-staged vs copied straight
+    into LDS, and the direct copies' stage count), and warm vs cold caches
+    for the layers whose working set fits the 256 MB last-level cache.
+    Median and min of 50 individually timed calls each."""
     rows = []
 
     def gemm_rows(ablation, case, variants):
@@ -485,9 +486,51 @@ def run_ablations(torch, pk, wl):
             ("256x256 tiles", "gemm_256x256x32_w2x4_nn_v44_o2"),
             ("128x128 tiles, persistent", "gemm_128x128x32_w2x4_nn_v44_o2_p")])
 
+    # operand staging: global -> registers -> LDS (ds_write) against global ->
+    # LDS directly (buffer_load ... lds), same tile and MFMA pipeline
+    gemm_rows("operand loader", g4096, [
+        ("register-staged 256x256x32", "gemm_256x256x32_w2x4_nn_v44_o2"),
+        ("direct-to-LDS 256x256x32, 2 stages", "gemm_256x256x32_w2x4_nn_v44_o2_dma2"),
+        ("register-staged 128x128x16", "gemm_128x128x16_w2x2_nn_v44"),
+        ("direct-to-LDS 128x128x16, 3 stages", "gemm_128x128x16_w2x2_nn_v44_dma3"),
+        ("register-staged 64x64x32", "gemm_64x64x32_w2x2_nn_v44"),
+        ("direct-to-LDS 64x64x32, 3 stages", "gemm_64x64x32_w2x2_nn_v44_dma3")])
+    gemm_rows("direct-to-LDS stages", g4096, [
+        ("2 stages 256x256x16", "gemm_256x256x16_w2x4_nn_v44_o2_dma2"),
+        ("3 stages 256x256x16", "gemm_256x256x16_w2x4_nn_v44_o2_dma3"),
+        ("4 stages 256x256x16", "gemm_256x256x16_w2x4_nn_v44_o2_dma4")])
+    by_name = {c.name: c for c in wl.STEP_CONVS}
+    for name, variants in (
+            ("vgg16 conv2_1 b32 112x112x64->128 3x3", [
+                ("register-staged 128x128x32", "conv_128x128x32_w2x4_v44_o2"),
+                ("direct-to-LDS 128x128x32, 2 stages", "conv_128x128x32_w2x4_v44_o2_dma2")]),
+            ("vgg16 conv3_1 b32 56x56x128->256 3x3", [
+                ("register-staged 128x128x32, stream-K", "conv_128x128x32_w2x4_v44_o2_sk"),
+                ("direct-to-LDS 128x128x32, stream-K", "conv_128x128x32_w2x4_v44_o2_dma2_sk")])):
+        case = by_name[name]
+        x, f = case.inputs()
+        N, H, W, Cin = case.x_shape
+        KH, KW, _, Cout = case.f_shape
+        Ho, Wo = case.out_hw
+        dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+        dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+        ws = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+        for label, cfg in variants:
+            pk.force_config(cfg)
+            try:
+                med, mn = _time_each(torch, lambda: pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads,
+                                                                  out=dy, workspace=ws))
+                used = pk.last_config_name()
+            finally:
+                pk.force_config(None)
+            rows.append({"ablation": "operand loader", "shape": name, "variant": label, "config": used,
+                         "ms_median": round(med, 4), "ms_min": round(mn, 4),
+                         "tflops": round(wl.conv_flops(case, Ho, Wo) / (med * 1e-3) / 1e12, 2)})
+            print("bench: operand loader %s %s %.4f ms" % (name, label, med), file=sys.stderr, flush=True)
+        del dx, df, dy, ws
+
     # warm vs cold: a 512 MiB scratch write between calls evicts L2 and MALL
     scratch = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
-    by_name = {c.name: c for c in wl.STEP_CONVS}
     for name in ("vgg16 conv1_1 b32 224x224x3->64 3x3", "resnet50 b32 56x56x64->64 1x1",
                  "resnet50 b32 56x56x64->256 1x1"):
         case = by_name[name]
