@@ -83,6 +83,11 @@ DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2,
        (128, 128, 32, 2, 4, 2, 2), (128, 128, 32, 2, 4, 3, 2), (128, 128, 32, 2, 4, 4, 2),
        (128, 128, 16, 2, 2, 3, 1), (128, 128, 16, 2, 2, 4, 1), (64, 64, 32, 2, 2, 3, 1)]
 
+# K-split forms of the direct-to-LDS contraction ("_kN_..._dmaS"): (BM, BN,
+# BK, WAVES_M, WAVES_N, groups, stages, OCC)
+DMA_KSPLIT = [(32, 64, 32, 1, 2, 4, 2, 1), (32, 64, 32, 1, 2, 4, 3, 1), (64, 64, 32, 2, 2, 2, 2, 1),
+              (64, 64, 32, 2, 2, 2, 3, 1), (32, 64, 16, 1, 2, 8, 3, 1)]
+
 # Stream-K forms of the direct-to-LDS contraction (NN GEMM and convolution).
 DMA_STREAMK = [(128, 128, 32, 2, 4, 2, 2), (128, 128, 16, 2, 2, 3, 1), (128, 128, 32, 2, 4, 3, 2)]
 
@@ -191,6 +196,13 @@ def main():
                            % ("gemm_%dx%dx%d_w%dx%d_%s_v44%s_dma%d" % (bm, bn, bk, wm, wn, layout,
                                                                      "_o%d" % occ if occ > 1 else "", st),
                               bm, bn, bk, wm, wn, st, ta, tb, occ))
+        for t in (DMA_KSPLIT if layout != "tt" else []):
+            bm, bn, bk, wm, wn, ks, st, occ = t
+            if (ta and bm % 64) or (not tb and bn % 64):
+                continue  # an m- or n-contiguous tile needs 64 columns for its swizzle
+            entries.append("PK_GEMM_DMA_KS(%s, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d)"
+                           % ("gemm_%dx%dx%d_w%dx%d_k%d_%s_v44_dma%d" % (bm, bn, bk, wm, wn, ks, layout, st),
+                              bm, bn, bk, wm, wn, ks, st, ta, tb, occ))
         for t in (DMA_STREAMK if layout == "nn" else []):
             bm, bn, bk, wm, wn, st, occ = t
             entries.append("PK_GEMM_DMA_SK(%s, %d, %d, %d, %d, %d, %d, %d)"

@@ -334,8 +334,10 @@ bool dma_fits(const Config *c, int64_t lda, int64_t ldb)
 //   - K <= 64: 64 x 64 tiles; for NN products with K == 64 and N a multiple
 //     of 64, the B-resident form (the whole reduction is one K-block);
 //   - longer reductions with at most one 32 x 64 tile per CU: the reduction
-//     split among 4 groups of 2 waves inside the work-group, loads two steps
-//     ahead (a lone work-group per CU walks a quarter of the K-blocks);
+//     split among 4 groups of 2 waves inside the work-group, each group's
+//     operands copied straight into three LDS stages (TN: register-staged,
+//     two steps ahead) -- a lone work-group per CU walks a quarter of the
+//     K-blocks;
 //     with at most one 64 x 64 tile per CU, 2 groups of 4 waves on 64 x 64
 //     tiles (the 64 .. 1024 sweep of M, N, K at K >= 128: 1.3-1.8x over
 //     one group, every shape);
@@ -375,7 +377,7 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64
         if (c && bres_fits(c, N, K, ldc)) return c;
         snprintf(name, sizeof(name), "gemm_64x64x16_w2x2_%s_v44", lay);
     } else if (ceil_div(M, 32) * ceil_div(N, 64) <= kCUs) {
-        snprintf(name, sizeof(name), "gemm_32x64x32_w1x2_k4_%s_v44_d2", lay);
+        return pick("gemm_32x64x32_w1x2_k4_%s_v44_dma3", "gemm_32x64x32_w1x2_k4_%s_v44_d2");
     } else if (ceil_div(M, 64) * ceil_div(N, 64) <= kCUs) {
         snprintf(name, sizeof(name), "gemm_64x64x32_w2x2_k2_%s_v44_d2", lay);
     } else if (ceil_div(M, 256) * ceil_div(N, 256) >= kCUs) {
@@ -447,16 +449,20 @@ int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 // CUs (a product that large is bound by its tiles' K loops, not by wave
 // quantization, and every split costs a pass over M x N partial sums), until
 // the work-groups fill about one round (K-split forms: one per CU; others:
-// two), keeping at least 8 K-blocks (K-split forms: two steps per group) per
-// split.
+// two), keeping at least 8 K-blocks (K-split forms: one step per group) per
+// split.  A K-split form splits only when each group would walk at least 4
+// steps without it: the reduce kernel's launch (about 2 us in a graph) costs
+// more than 1 step saved (the GEMM sweep: at K = 256 a split of 2 loses up
+// to 1.25x; at K = 512, 4 splits beat none by up to 0.9 us).
 int gemm_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 {
     if (c->bres) return 1;
     const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
     const int64_t nkb = ceil_div(K, c->bk);
     if (tiles >= kCUs) return 1;
+    if (c->kgroups > 1 && nkb < 4 * c->kgroups) return 1;
     int64_t s = ceil_div((c->kgroups > 1 ? 1 : 2) * kCUs, tiles);
-    const int64_t max_by_k = nkb / (c->kgroups > 1 ? 2 * c->kgroups : 8);
+    const int64_t max_by_k = nkb / (c->kgroups > 1 ? c->kgroups : 8);
     if (s > max_by_k) s = max_by_k;
     if (s > 16) s = 16;
     return s < 1 ? 1 : (int)s;

@@ -1536,6 +1536,152 @@ gemm_streamk_kernel(KernelArgs p)
 }
 
 
+// The K-split contraction (groups of waves splitting each tile's K-blocks,
+// as gemm_ksplit_kernel) with every group's operand tiles copied straight
+// into its own STAGES LDS stages (DmaOperand), so each group has S-1 of its
+// K-blocks in flight at no register cost -- for products with few tiles and
+// a long reduction, whose time is the chain of a group's K-blocks.  A group
+// past the split's last K-block copies zeros (k bounded by the split).  All
+// groups take the same number of steps, so the work-group's barriers line
+// up; at the end the partial tiles are added through LDS in group order.
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int KS, int STAGES, int AMODE, bool TB, int OCC,
+          bool BETA>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N * KS) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+gemm_dma_ksplit_kernel(KernelArgs p)
+{
+    typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, false, 4, 4> G;  // MFMA and epilogue only
+    static_assert(AMODE != A_CONV, "dense operands only");
+    constexpr int GT = G::NT, NW = GT / 64;  // threads and waves per group
+    typedef DmaOperand<BM, BK, NW, AMODE == A_KCONTIG> OpA;
+    typedef DmaOperand<BN, BK, NW, TB> OpB;
+    constexpr int A_ST = OpA::FLOATS, B_ST = OpB::FLOATS;
+    constexpr int GSTAGES = STAGES * (A_ST + B_ST);  // floats of one group's stages
+    constexpr int LPB = OpA::L + OpB::L;
+    constexpr int ACCF = G::RM * G::RN * 16;  // accumulator floats per lane
+    static_assert(STAGES >= 2 && STAGES <= 4, "two to four LDS stages");
+    static_assert((STAGES - 2) * LPB <= 63, "vmcnt range");
+    static_assert((KS - 1) * GT * ACCF <= KS * GSTAGES, "partial tiles fit in the stages");
+
+    __shared__ __attribute__((aligned(16))) float smem[KS * GSTAGES];
+
+    const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x / GT);
+    const int tid = threadIdx.x - grp * GT;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // within the group
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int l32 = lane & 31, h = lane >> 5;
+    float *gs = smem + grp * GSTAGES;
+
+    if (p.nbatch > 1) {  // product blockIdx.y of a batch
+        const int64_t bz = blockIdx.y;
+        p.A += bz * p.stride_a;
+        p.B += bz * p.stride_b;
+        p.C += bz * p.stride_c;
+    }
+    int tm, tn;
+    tile_coords(p, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    int kbeg, kend;  // K-blocks of this work-group's split
+    split_range(p, BK, blockIdx.z, kbeg, kend);
+    const int steps = (kend - kbeg + KS - 1) / KS;  // K-block steps of every group
+    const int klim = min(p.K, kend * BK);          // k past the split reads as zero
+
+    OpA oa;
+    OpB ob;
+    oa.init(p.lda, m0, p.M, wave, lane);
+    ob.init(p.ldb, n0, p.N, wave, lane);
+    // step st of group g is K-block kbeg + st*KS + g
+    auto issue = [&](int st, int s) {
+        const int k0 = (kbeg + st * KS + grp) * BK;
+        float *as = gs + s * (A_ST + B_ST);
+        oa.issue(p.A, p.lda, m0, k0, klim, as, wave);
+        ob.issue(p.B, p.ldb, n0, k0, klim, as + A_ST, wave);
+    };
+    auto wait_blocks = [&](int later) {
+        if (STAGES >= 4 && later >= 2)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPB) : "memory");
+        else if (STAGES >= 3 && later >= 1)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPB) : "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+    auto barrier = [] {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    const int a_row = wm * G::WM + l32;
+    const int b_row = wn * G::WN + l32;
+    auto read_group = [&](const float *as, int g, typename G::FragA &xa, typename G::FragB &xb) {
+#pragma unroll
+        for (int i = 0; i < G::RM; ++i) OpA::read4(as, a_row + i * 32, h, g, xa[i]);
+#pragma unroll
+        for (int j = 0; j < G::RN; ++j) OpB::read4(as + A_ST, b_row + j * 32, h, g, xb[j]);
+    };
+
+    typename G::Acc acc;
+    G::zero(acc);
+    typename G::FragA fa[2];
+    typename G::FragB fb[2];
+    constexpr int NG = G::NG;
+
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < steps) issue(s, s);
+    wait_blocks(min(STAGES - 2, steps - 1));
+    barrier();
+    if (steps > 0) read_group(gs, 0, fa[0], fb[0]);
+
+    int s = 0;
+    for (int st = 0; st < steps; ++st) {
+        const int s_next = s + 1 == STAGES ? 0 : s + 1;
+        if (st + STAGES - 1 < steps) issue(st + STAGES - 1, s == 0 ? STAGES - 1 : s - 1);
+        const float *as = gs + s * (A_ST + B_ST);
+#pragma unroll
+        for (int g = 0; g < NG - 1; ++g) {
+            read_group(as, g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            G::mma_group(acc, fa[g & 1], fb[g & 1]);
+        }
+        wait_blocks(min(STAGES - 2, steps - st - 2));
+        barrier();
+        // unconditional (stale after the last step, never used)
+        read_group(gs + s_next * (A_ST + B_ST), 0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        G::mma_group(acc, fa[(NG - 1) & 1], fb[(NG - 1) & 1]);
+        s = s_next;
+    }
+
+    // every copy has landed and every stage read is done before the partial
+    // tiles of groups 1..KS-1 overwrite the stages; group 0 adds them in
+    // group order and writes C
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    barrier();
+    if (grp > 0) {
+        float *slot = smem + (grp - 1) * GT * ACCF + tid;
+#pragma unroll
+        for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+            for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) slot[((i * G::RN + j) * 16 + r) * GT] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+        for (int q = 1; q < KS; ++q) {
+            const float *slot = smem + (q - 1) * GT * ACCF + tid;
+#pragma unroll
+            for (int i = 0; i < G::RM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::RN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[i][j][r] += slot[((i * G::RN + j) * 16 + r) * GT];
+        }
+        G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+    }
+}
+
 // Stream-K form of the direct-to-LDS contraction: the grid is the resident
 // work-groups and each walks its share of the (tile, K-block) iterations as
 // gemm_streamk_kernel does, with the copies issued STAGES-1 iterations ahead

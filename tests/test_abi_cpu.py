@@ -233,7 +233,7 @@ def test_config_space(pk):
         assert c["bk"] % 8 == 0
         if c["dma"]:  # unpadded, swizzled tiles copied straight into 2 to 4 LDS stages
             assert c["kind"] in (0, 1) and c["stages"] in (2, 3, 4) and c["vec_a"] == c["vec_b"] == 4
-            assert c["lds_bytes"] == c["stages"] * 4 * (c["bm"] * c["bk"] + c["bk"] * c["bn"]), c["name"]
+            assert c["lds_bytes"] == c["kgroups"] * c["stages"] * 4 * (c["bm"] * c["bk"] + c["bk"] * c["bn"]), c["name"]
             assert c["name"].endswith("_dma%d" % c["stages"]) or c["name"].endswith("_dma%d_sk" % c["stages"])
             continue
         assert c["stages"] in (1, 2)
