@@ -155,6 +155,38 @@ def test_winograd_argument_checks(pk):
     assert call(N=0) == 0
 
 
+def test_direct_to_lds_range_checks(pk):
+    """The direct-to-LDS forms address one tile's rows of each operand (and
+    a convolution's whole image) in 32-bit byte offsets: a forced one is
+    refused (PK_ERR_NOT_SUPPORTED) when those rows span 2 GiB or more, and
+    accepted up to the launch below that; every call fails before a kernel
+    launches (no GPU here), so the refusal is the range check's."""
+    from paper_1904_05347_amd import binding
+    fake = 0x100000
+    big_lda = (1 << 31) // (4 * 256) + 4  # 256 rows of A span just over 2 GiB
+    pk.force_config("gemm_256x256x32_w2x4_nn_v44_o2_dma2")
+    try:
+        st = binding.sgemm("N", "N", 256, 256, 64, 1.0, fake, big_lda, fake + (1 << 40), 256, 0.0,
+                           fake + (2 << 40), 256)
+        assert st == 2
+        # transposed A: BK rows of lda floats per tile, far below the limit
+        pk.force_config("gemm_256x256x32_w2x4_tn_v44_o2_dma2")
+        st = binding.sgemm("T", "N", 256, 256, 64, 1.0, fake, big_lda, fake + (1 << 40), 256, 0.0,
+                           fake + (2 << 40), 256)
+        assert st != 2
+    finally:
+        pk.force_config(None)
+    # convolution: an image of 2 GiB or more
+    pk.force_config("conv_128x128x32_w2x4_v44_o2_dma2")
+    try:
+        N, H, W, Cin, Cout = 64, 128, 128, 512, 128  # 4 * N*H*W*Cin = 2 GiB
+        st = binding.conv2d_fwd_raw(fake, N, H, W, Cin, fake + (1 << 42), 3, 3, Cout, 1, 1, 1, 1, 1, 1,
+                                    fake + (2 << 42), H, W)
+        assert st == 2
+    finally:
+        pk.force_config(None)
+
+
 def test_gemm_workspace_checks(pk):
     """pk_sgemm_ws: a forced split needs workspace for every slice
     (PK_ERR_WORKSPACE), the workspace must not overlap A, B or C (position 14),
