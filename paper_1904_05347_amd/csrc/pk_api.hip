@@ -1087,8 +1087,6 @@ bool wino_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Cin, int64_t Cout, Win
 // to Cin = 128 and of 32 beyond.
 const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok, bool *bad)
 {
-    (void)T;
-    (void)Cout;
     const Config *c = forced(bad);
     if (*bad) return nullptr;
     // the 16 products are (T x Cin) (Cin x Cout), lda = Cin, ldb = Cout
@@ -1097,7 +1095,15 @@ const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok
                    ? c
                    : nullptr;
     if (!vec_ok) return find_config("gemm_64x64x16_w2x2_nn_v11");
-    return find_config(Cin <= 128 ? "gemm_64x64x16_w2x2_nn_v44" : "gemm_64x64x32_w2x2_nn_v44");
+    if (Cin <= 128) return find_config("gemm_64x64x16_w2x2_nn_v44");
+    // deeper channels: operands copied straight into LDS; 128 x 128 tiles
+    // once the 16 products hold 4 of them per CU (VGG-16 conv3_2 .. conv4_2
+    // at batch 32: 0.93-0.95x the time of the register-staged 64 x 64 x 32),
+    // else 64 x 64 x 32 in three stages (0.93-0.98x)
+    const bool big = 16 * ceil_div(T, 128) * ceil_div(Cout, 128) >= 4 * kCUs;
+    const Config *c2 = find_config(big ? "gemm_128x128x32_w2x4_nn_v44_o2_dma2" : "gemm_64x64x32_w2x2_nn_v44_dma3");
+    if (c2 && dma_fits(c2, Cin, Cout)) return c2;
+    return find_config("gemm_64x64x32_w2x2_nn_v44");
 }
 
 }  // namespace
