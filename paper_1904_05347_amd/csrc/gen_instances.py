@@ -88,6 +88,10 @@ DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2,
 DMA_KSPLIT = [(32, 64, 32, 1, 2, 4, 2, 1), (32, 64, 32, 1, 2, 4, 3, 1), (64, 64, 32, 2, 2, 2, 2, 1),
               (64, 64, 32, 2, 2, 2, 3, 1), (32, 64, 16, 1, 2, 8, 3, 1)]
 
+# ... and for the convolution's gather: few output tiles, long reductions
+# (deep layers at small batch, strided 1x1 layers).
+DMA_KSPLIT_CONV = [(64, 64, 32, 2, 2, 2, 3, 1), (64, 64, 32, 2, 2, 4, 2, 1), (128, 128, 32, 2, 2, 2, 2, 1)]
+
 # Stream-K forms of the direct-to-LDS contraction (NN GEMM and convolution).
 DMA_STREAMK = [(128, 128, 32, 2, 4, 2, 2), (128, 128, 16, 2, 2, 3, 1), (128, 128, 32, 2, 4, 3, 2)]
 
@@ -243,6 +247,11 @@ def main():
         entries.append("PK_CONV_DMA(%s, %d, %d, %d, %d, %d, %d, %d)"
                        % ("conv_%dx%dx%d_w%dx%d_v44%s_dma%d" % (bm, bn, bk, wm, wn, "_o%d" % occ if occ > 1 else "", st),
                           bm, bn, bk, wm, wn, st, occ))
+    for t in DMA_KSPLIT_CONV:
+        bm, bn, bk, wm, wn, ks, st, occ = t
+        entries.append("PK_CONV_DMA_KS(%s, %d, %d, %d, %d, %d, %d, %d, %d)"
+                       % ("conv_%dx%dx%d_w%dx%d_k%d_v44_dma%d" % (bm, bn, bk, wm, wn, ks, st),
+                          bm, bn, bk, wm, wn, ks, st, occ))
     for t in DMA_STREAMK:
         bm, bn, bk, wm, wn, st, occ = t
         entries.append("PK_CONV_DMA_SK(%s, %d, %d, %d, %d, %d, %d, %d)"

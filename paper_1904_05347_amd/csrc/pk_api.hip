@@ -168,7 +168,9 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv5_1 b32 14x14x512->512 3x3 s1
     {1, 0, 0, 401408, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b32 230x230x3->64 7x7 s2
     {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},  // resnet50 conv2_1 b32 56x56x64->256 1x1 s1
-    {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv2_2 b32 56x56x64->64 1x1 s1 (in the step: the B-resident form is faster alone, slower there)
+    // (kept by hand: inside the benchmark step the B-resident and direct-to-LDS
+    // forms, faster alone, take 20.0-20.1 us against this one's 19.5)
+    {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv2_2 b32 56x56x64->64 1x1 s1
     {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // resnet50 conv2_3 b32 56x56x64->64 3x3 s1
     {1, 0, 0, 100352, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_4 b32 56x56x256->64 1x1 s1
     {1, 0, 0, 25088, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv2_5 b32 56x56x64->64 3x3 s2
@@ -196,11 +198,11 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 50176, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // vgg16 conv1_2 b1 224x224x64->64 3x3 s1
     {1, 0, 0, 12544, 128, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv2_1 b1 112x112x64->128 3x3 s1
     {1, 0, 0, 12544, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv2_2 b1 112x112x128->128 3x3 s1
-    {1, 0, 0, 3136, 256, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv3_1 b1 56x56x128->256 3x3 s1
-    {1, 0, 0, 3136, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // vgg16 conv3_2 b1 56x56x256->256 3x3 s1
-    {1, 0, 0, 784, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 9},  // vgg16 conv4_1 b1 28x28x256->512 3x3 s1
+    {1, 0, 0, 3136, 256, 1152, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 1},  // vgg16 conv3_1 b1 56x56x128->256 3x3 s1
+    {1, 0, 0, 3136, 256, 2304, 3, 1, "conv_64x64x32_w2x2_k4_v44_dma2", 1},  // vgg16 conv3_2 b1 56x56x256->256 3x3 s1
+    {1, 0, 0, 784, 512, 2304, 3, 1, "conv_64x64x32_w2x2_k4_v44_dma2", 2},  // vgg16 conv4_1 b1 28x28x256->512 3x3 s1
     {1, 0, 0, 784, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 12},  // vgg16 conv4_2 b1 28x28x512->512 3x3 s1
-    {1, 0, 0, 196, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 8},  // vgg16 conv5_1 b1 14x14x512->512 3x3 s1
+    {1, 0, 0, 196, 512, 4608, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 8},  // vgg16 conv5_1 b1 14x14x512->512 3x3 s1
     {1, 0, 0, 200704, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b4 224x224x3->64 3x3 s1
     {1, 0, 0, 200704, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv1_2 b4 224x224x64->64 3x3 s1
     {1, 0, 0, 50176, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // vgg16 conv2_1 b4 112x112x64->128 3x3 s1
@@ -211,52 +213,52 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 3136, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_2 b4 28x28x512->512 3x3 s1
     {1, 0, 0, 12544, 64, 147, 7, 2, "conv_64x64x16_w2x2_v11", 1},  // resnet50 conv1_1 b1 230x230x3->64 7x7 s2
     {1, 0, 0, 3136, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b1 56x56x64->256 1x1 s1
-    {1, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
-    {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 3},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
-    {1, 0, 0, 3136, 64, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
+    {1, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
+    {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 3},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
+    {1, 0, 0, 3136, 64, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
     {1, 0, 0, 784, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 8},  // resnet50 conv2_5 b1 56x56x64->64 3x3 s2
     {1, 0, 0, 784, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b1 28x28x64->256 1x1 s1
-    {1, 0, 0, 784, 512, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
-    {1, 0, 0, 784, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
-    {1, 0, 0, 784, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv3_4 b1 28x28x128->128 3x3 s1
+    {1, 0, 0, 784, 512, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
+    {1, 0, 0, 784, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
+    {1, 0, 0, 784, 128, 1152, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 6},  // resnet50 conv3_4 b1 28x28x128->128 3x3 s1
     {1, 0, 0, 784, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv3_5 b1 28x28x128->512 1x1 s1
     {1, 0, 0, 784, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv3_6 b1 28x28x512->128 1x1 s1
     {1, 0, 0, 196, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv3_7 b1 28x28x128->128 3x3 s2
     {1, 0, 0, 196, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv4_1 b1 14x14x128->512 1x1 s1
-    {1, 0, 0, 196, 1024, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
+    {1, 0, 0, 196, 1024, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
     {1, 0, 0, 196, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
-    {1, 0, 0, 196, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 12},  // resnet50 conv4_4 b1 14x14x256->256 3x3 s1
-    {1, 0, 0, 196, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
-    {1, 0, 0, 196, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 4},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
+    {1, 0, 0, 196, 256, 2304, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 12},  // resnet50 conv4_4 b1 14x14x256->256 3x3 s1
+    {1, 0, 0, 196, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
+    {1, 0, 0, 196, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
     {1, 0, 0, 49, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv4_7 b1 14x14x256->256 3x3 s2
-    {1, 0, 0, 49, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
+    {1, 0, 0, 49, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
     {1, 0, 0, 49, 2048, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 8},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
-    {1, 0, 0, 49, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 8},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
+    {1, 0, 0, 49, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 8},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
     {1, 0, 0, 49, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv5_4 b1 7x7x512->512 3x3 s1
     {1, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
-    {1, 0, 0, 49, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 8},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
+    {1, 0, 0, 49, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 8},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
     {1, 0, 0, 50176, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b4 230x230x3->64 7x7 s2
     {1, 0, 0, 12544, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b4 56x56x64->256 1x1 s1
-    {1, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
-    {1, 0, 0, 12544, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv2_3 b4 56x56x64->64 3x3 s1
-    {1, 0, 0, 12544, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_4 b4 56x56x256->64 1x1 s1
+    {1, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
+    {1, 0, 0, 12544, 64, 576, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 1},  // resnet50 conv2_3 b4 56x56x64->64 3x3 s1
+    {1, 0, 0, 12544, 64, 256, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv2_4 b4 56x56x256->64 1x1 s1
     {1, 0, 0, 3136, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 3},  // resnet50 conv2_5 b4 56x56x64->64 3x3 s2
     {1, 0, 0, 3136, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_2 b4 28x28x256->512 1x1 s1
-    {1, 0, 0, 3136, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_3 b4 28x28x256->128 1x1 s1
-    {1, 0, 0, 3136, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 4},  // resnet50 conv3_4 b4 28x28x128->128 3x3 s1
+    {1, 0, 0, 3136, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_3 b4 28x28x256->128 1x1 s1
+    {1, 0, 0, 3136, 128, 1152, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 2},  // resnet50 conv3_4 b4 28x28x128->128 3x3 s1
     {1, 0, 0, 3136, 512, 128, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_5 b4 28x28x128->512 1x1 s1
-    {1, 0, 0, 3136, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv3_6 b4 28x28x512->128 1x1 s1
-    {1, 0, 0, 784, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv3_7 b4 28x28x128->128 3x3 s2
-    {1, 0, 0, 784, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_2 b4 14x14x512->1024 1x1 s1
-    {1, 0, 0, 784, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv4_3 b4 14x14x512->256 1x1 s1
-    {1, 0, 0, 784, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 9},  // resnet50 conv4_4 b4 14x14x256->256 3x3 s1
-    {1, 0, 0, 784, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_5 b4 14x14x256->1024 1x1 s1
-    {1, 0, 0, 784, 256, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 4},  // resnet50 conv4_6 b4 14x14x1024->256 1x1 s1
-    {1, 0, 0, 196, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 12},  // resnet50 conv4_7 b4 14x14x256->256 3x3 s2
-    {1, 0, 0, 196, 2048, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 4},  // resnet50 conv5_2 b4 7x7x1024->2048 1x1 s1
-    {1, 0, 0, 196, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 4},  // resnet50 conv5_3 b4 7x7x1024->512 1x1 s1
-    {1, 0, 0, 196, 2048, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 1},  // resnet50 conv5_5 b4 7x7x512->2048 1x1 s1
-    {1, 0, 0, 196, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 4},  // resnet50 conv5_6 b4 7x7x2048->512 1x1 s1
+    {1, 0, 0, 3136, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma2", 1},  // resnet50 conv3_6 b4 28x28x512->128 1x1 s1
+    {1, 0, 0, 784, 128, 1152, 3, 2, "conv_64x64x32_w2x2_k2_v44_dma3", 6},  // resnet50 conv3_7 b4 28x28x128->128 3x3 s2
+    {1, 0, 0, 784, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv4_2 b4 14x14x512->1024 1x1 s1
+    {1, 0, 0, 784, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_3 b4 14x14x512->256 1x1 s1
+    {1, 0, 0, 784, 256, 2304, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 4},  // resnet50 conv4_4 b4 14x14x256->256 3x3 s1
+    {1, 0, 0, 784, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv4_5 b4 14x14x256->1024 1x1 s1
+    {1, 0, 0, 784, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 2},  // resnet50 conv4_6 b4 14x14x1024->256 1x1 s1
+    {1, 0, 0, 196, 256, 2304, 3, 2, "conv_64x64x32_w2x2_k2_v44_dma3", 12},  // resnet50 conv4_7 b4 14x14x256->256 3x3 s2
+    {1, 0, 0, 196, 2048, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma2", 1},  // resnet50 conv5_2 b4 7x7x1024->2048 1x1 s1
+    {1, 0, 0, 196, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv5_3 b4 7x7x1024->512 1x1 s1
+    {1, 0, 0, 196, 2048, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv5_5 b4 7x7x512->2048 1x1 s1
+    {1, 0, 0, 196, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv5_6 b4 7x7x2048->512 1x1 s1
     // ResNet-50 56x56x256 1x1 stride 2 -> 128 at batch 32 (the benchmark step's
     // reading of that layer; not a row of the paper's table)
     {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x32_w2x4_v44_o2_dma3", 1},

@@ -144,11 +144,13 @@ static hipError_t launch_gemm_dma_ksplit(const KernelArgs &a, hipStream_t stream
 {
     const dim3 grid((unsigned)(a.tiles_m * a.tiles_n), (unsigned)(a.nbatch > 1 ? a.nbatch : 1), (unsigned)a.splits);
     const dim3 block(64 * WAVES_M * WAVES_N * KS);
-    if (reads_c<AMODE>(a)) {
-        hipLaunchKernelGGL(
-            (gemm_dma_ksplit_kernel<BM, BN, BK, WAVES_M, WAVES_N, KS, STAGES, AMODE, TB, OCC, true>), grid, block,
-            0, stream, a);
-        return hipGetLastError();
+    if constexpr (AMODE != A_CONV) {
+        if (reads_c<AMODE>(a)) {
+            hipLaunchKernelGGL(
+                (gemm_dma_ksplit_kernel<BM, BN, BK, WAVES_M, WAVES_N, KS, STAGES, AMODE, TB, OCC, true>), grid,
+                block, 0, stream, a);
+            return hipGetLastError();
+        }
     }
     hipLaunchKernelGGL((gemm_dma_ksplit_kernel<BM, BN, BK, WAVES_M, WAVES_N, KS, STAGES, AMODE, TB, OCC, false>),
                        grid, block, 0, stream, a);
@@ -308,6 +310,10 @@ static constexpr int lds_bytes()
     {#name, KIND_GEMM, BM, BN, BK, WM, WN, TA, TB, 4, 4, OCC, 0, KS * STAGES * 4 * (BM * BK + BK * BN), \
      &launch_gemm_dma_ksplit<BM, BN, BK, WM, WN, KS, STAGES, (TA ? A_MCONTIG : A_KCONTIG), (TB != 0), OCC>, \
      0, 0, nullptr, 0, KS, STAGES}
+
+#define PK_CONV_DMA_KS(name, BM, BN, BK, WM, WN, KS, STAGES, OCC)                                    \
+    {#name, KIND_CONV, BM, BN, BK, WM, WN, 0, 0, 4, 4, OCC, 0, KS * STAGES * 4 * (BM * BK + BK * BN),     \
+     &launch_gemm_dma_ksplit<BM, BN, BK, WM, WN, KS, STAGES, A_CONV, false, OCC>, 0, 0, nullptr, 0, KS, STAGES}
 
 #define PK_GEMM_DMA_SK(name, BM, BN, BK, WM, WN, STAGES, OCC)                                       \
     {#name, KIND_GEMM, BM, BN, BK, WM, WN, 0, 0, 4, 4, OCC, 0, STAGES * 4 * (BM * BK + BK * BN),       \

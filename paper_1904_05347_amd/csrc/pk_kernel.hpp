@@ -698,8 +698,9 @@ struct DmaConvA {
         kh = tap / KW;
         kw = tap - kh * KW;
     }
-    // copy K-block k0 (the one the walk stands at) into `tile`, then step the walk
-    __device__ __forceinline__ void issue(const float *x, int k0, int K, float *tile, int wave)
+    // copy K-block k0 (the one the walk stands at) into `tile`, then step the
+    // walk `blocks` K-blocks on
+    __device__ __forceinline__ void issue(const float *x, int k0, int K, float *tile, int wave, int blocks = 1)
     {
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)x, 0, 0x7fffffff, 0x00020000);
         const bool k_ok = k0 + col < K;
@@ -711,7 +712,7 @@ struct DmaConvA {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rs, (__attribute__((address_space(3))) void *)(tile + (i * NW + wave) * 256), 16, o, 0, 0, 0);
         }
-        ci += BK;
+        ci += BK * blocks;
         while (ci >= Cin) {
             ci -= Cin;
             if (++kw == KW) { kw = 0; ++kh; }
@@ -1550,9 +1551,9 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N * KS) __attribute__((am
 gemm_dma_ksplit_kernel(KernelArgs p)
 {
     typedef GemmTile<BM, BN, BK, WAVES_M, WAVES_N, A_KCONTIG, false, 4, 4> G;  // MFMA and epilogue only
-    static_assert(AMODE != A_CONV, "dense operands only");
     constexpr int GT = G::NT, NW = GT / 64;  // threads and waves per group
-    typedef DmaOperand<BM, BK, NW, AMODE == A_KCONTIG> OpA;
+    typedef typename std::conditional<AMODE == A_CONV, DmaConvA<BM, BK, NW>,
+                                      DmaOperand<BM, BK, NW, AMODE == A_KCONTIG>>::type OpA;
     typedef DmaOperand<BN, BK, NW, TB> OpB;
     constexpr int A_ST = OpA::FLOATS, B_ST = OpB::FLOATS;
     constexpr int GSTAGES = STAGES * (A_ST + B_ST);  // floats of one group's stages
@@ -1572,11 +1573,13 @@ gemm_dma_ksplit_kernel(KernelArgs p)
     const int l32 = lane & 31, h = lane >> 5;
     float *gs = smem + grp * GSTAGES;
 
-    if (p.nbatch > 1) {  // product blockIdx.y of a batch
-        const int64_t bz = blockIdx.y;
-        p.A += bz * p.stride_a;
-        p.B += bz * p.stride_b;
-        p.C += bz * p.stride_c;
+    if constexpr (AMODE != A_CONV) {
+        if (p.nbatch > 1) {  // product blockIdx.y of a batch
+            const int64_t bz = blockIdx.y;
+            p.A += bz * p.stride_a;
+            p.B += bz * p.stride_b;
+            p.C += bz * p.stride_c;
+        }
     }
     int tm, tn;
     tile_coords(p, tm, tn);
@@ -1588,13 +1591,19 @@ gemm_dma_ksplit_kernel(KernelArgs p)
 
     OpA oa;
     OpB ob;
-    oa.init(p.lda, m0, p.M, wave, lane);
+    if constexpr (AMODE == A_CONV)
+        oa.init(p, m0, kbeg + grp, wave, lane);  // the gather walks this group's K-blocks, KS apart
+    else
+        oa.init(p.lda, m0, p.M, wave, lane);
     ob.init(p.ldb, n0, p.N, wave, lane);
-    // step st of group g is K-block kbeg + st*KS + g
+    // step st of group g is K-block kbeg + st*KS + g; steps are issued in order
     auto issue = [&](int st, int s) {
         const int k0 = (kbeg + st * KS + grp) * BK;
         float *as = gs + s * (A_ST + B_ST);
-        oa.issue(p.A, p.lda, m0, k0, klim, as, wave);
+        if constexpr (AMODE == A_CONV)
+            oa.issue(p.A, k0, klim, as, wave, KS);
+        else
+            oa.issue(p.A, p.lda, m0, k0, klim, as, wave);
         ob.issue(p.B, p.ldb, n0, k0, klim, as + A_ST, wave);
     };
     auto wait_blocks = [&](int later) {

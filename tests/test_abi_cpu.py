@@ -257,7 +257,7 @@ def test_config_space(pk):
     assert len(set(names)) == len(names)
     for c in cfgs:
         assert c["threads"] == 64 * c["waves_m"] * c["waves_n"] * c["kgroups"]
-        assert c["kgroups"] == 1 or (c["kind"] == 0 and not c["persistent"] and not c["streamk"])
+        assert c["kgroups"] == 1 or (c["kind"] in (0, 1) and not c["persistent"] and not c["streamk"])
         assert c["lds_bytes"] <= 160 * 1024
         if c["kind"] == 2:  # tiled direct convolution: one LDS input patch
             continue
