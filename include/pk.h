@@ -288,13 +288,16 @@ int pk_get_config(int idx, pk_config_info *info);
  * PK_ERR_NOT_SUPPORTED.  Unknown names give PK_ERR_INVALID_VALUE.  The
  * environment variable PK_FORCE_CONFIG, read at first use, sets the same
  * override for threads that never call this; if it names no configuration,
- * every pk_sgemm / pk_conv2d_fwd call returns PK_ERR_INVALID_VALUE with
+ * every pk_sgemm(_ws) / pk_conv2d_fwd call returns PK_ERR_INVALID_VALUE with
  * pk_last_invalid_param() == 0.
  */
 int pk_force_config(const char *name);
 
-/* Forces the split factor of later convolution calls on this thread
- * (0 restores the selector's choice). */
+/* Forces the split of the reduction across work-groups of later
+ * pk_sgemm_ws and convolution calls on this thread (0 restores the
+ * selector's choice; 1 = no split).  A forced split needs workspace for
+ * every slice (else PK_ERR_WORKSPACE); B-resident configurations take none
+ * (PK_ERR_NOT_SUPPORTED); stream-K configurations ignore it. */
 int pk_force_splits(int splits);
 
 /*
