@@ -50,7 +50,8 @@ def parse():
                          "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
                          "the vendor fp32 GEMM beside it; winograd: the 3x3 stride-1 layers through the "
                          "Winograd F(2x2, 3x3) path beside the default path; ablations: double buffering, "
-                         "vector width, wave-tile shape, tile size vs CU fill, warm vs cold caches; tune: "
+                         "vector width, wave-tile shape, tile size vs CU fill, operand loader, the convolution's "
+                         "gather vs a dense operand, warm vs cold caches; tune: "
                          "the automated parameter search against the built-in choices")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
@@ -438,9 +439,12 @@ def run_ablations(torch, pk, wl):
     buffering (two LDS stages vs one), load vector width (16/8/4 bytes),
     square vs elongated wave tiles at equal accumulator count, tile size
     against CU fill, the operand loader (register-staged vs copied straight
-    into LDS, and the direct copies' stage count), and warm vs cold caches
-    for the layers whose working set fits the 256 MB last-level cache.
-    Median and min of 50 individually timed calls each."""
+    into LDS, and the direct copies' stage count), the convolution's gather
+    against a dense operand of the same shape, and warm vs cold caches for
+    the layers whose working set fits the 256 MB last-level cache.  Median
+    and min of 50 individually timed calls each."""
+    import numpy as np
+
     rows = []
 
     def gemm_rows(ablation, case, variants):
@@ -528,6 +532,49 @@ def run_ablations(torch, pk, wl):
                          "tflops": round(wl.conv_flops(case, Ho, Wo) / (med * 1e-3) / 1e12, 2)})
             print("bench: operand loader %s %s %.4f ms" % (name, label, med), file=sys.stderr, flush=True)
         del dx, df, dy, ws
+
+    # what the convolution's gather costs: each VGG layer against a dense NN
+    # GEMM of its implicit-GEMM shape (M = N*Ho*Wo, N = Cout, K = KH*KW*Cin)
+    # on the same tile and pipeline, and the same layer on 256x256 tiles
+    for name, forms in (
+            ("vgg16 conv2_1 b32 112x112x64->128 3x3", [
+                ("128x128x32, 2 stages", "conv_128x128x32_w2x4_v44_o2_dma2", "gemm_128x128x32_w2x4_nn_v44_o2_dma2"),
+                ("256x256x32, 2 stages", "conv_256x256x32_w2x4_v44_o2_dma2", "gemm_256x256x32_w2x4_nn_v44_o2_dma2")]),
+            ("vgg16 conv4_1 b32 28x28x256->512 3x3", [
+                ("128x128x32, stream-K", "conv_128x128x32_w2x4_v44_o2_dma2_sk",
+                 "gemm_128x128x32_w2x4_nn_v44_o2_dma2_sk"),
+                ("256x256x32, 2 stages", "conv_256x256x32_w2x4_v44_o2_dma2", "gemm_256x256x32_w2x4_nn_v44_o2_dma2")])):
+        case = by_name[name]
+        x, f = case.inputs()
+        N, H, W, Cin = case.x_shape
+        KH, KW, _, Cout = case.f_shape
+        Ho, Wo = case.out_hw
+        M, K = N * Ho * Wo, KH * KW * Cin
+        rng = np.random.default_rng(M + K)
+        dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+        dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+        dA = torch.from_numpy(wl.uniform(rng, M * K).reshape(M, K)).cuda()
+        dB = torch.from_numpy(wl.uniform(rng, K * Cout).reshape(K, Cout)).cuda()
+        dC = torch.empty((M, Cout), dtype=torch.float32, device="cuda")
+        ws = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+        fl = wl.conv_flops(case, Ho, Wo)
+        for label, conv_cfg, gemm_cfg in forms:
+            for what, cfg, fn in (
+                    ("convolution (gathered A)", conv_cfg,
+                     lambda: pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads, out=dy, workspace=ws)),
+                    ("dense GEMM %dx%dx%d" % (M, Cout, K), gemm_cfg, lambda: pk.gemm(dA, dB, dC, workspace=ws))):
+                pk.force_config(cfg)
+                try:
+                    med, mn = _time_each(torch, fn)
+                    used = pk.last_config_name()
+                finally:
+                    pk.force_config(None)
+                rows.append({"ablation": "gather vs dense A", "shape": name, "variant": "%s, %s" % (what, label),
+                             "config": used, "ms_median": round(med, 4), "ms_min": round(mn, 4),
+                             "tflops": round(fl / (med * 1e-3) / 1e12, 2)})
+                print("bench: gather vs dense %s %s %s %.4f ms" % (name, what, label, med), file=sys.stderr,
+                      flush=True)
+        del dx, df, dy, dA, dB, dC, ws
 
     # warm vs cold: a 512 MiB scratch write between calls evicts L2 and MALL
     scratch = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
