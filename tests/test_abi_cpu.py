@@ -301,3 +301,16 @@ def test_force_config_and_status_strings(pk):
     for s in range(5):
         assert lib.pk_status_string(s)
     assert pk.conv2d_workspace_bytes(32, 7, 7, 2048, 3, 3, 512, 1, 1, 1, 1, 1, 1) >= 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """Without libpk.so the package raises instead of computing anything:
+    there is no other compute path to fall back to."""
+    import paper_1904_05347_amd as pkg
+    from paper_1904_05347_amd import binding
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "libpk.so"))
+    monkeypatch.setattr(binding, "_lib", None)
+    with pytest.raises(pkg.PkLibraryMissing):
+        pkg.load()
+    with pytest.raises(pkg.PkLibraryMissing):
+        pkg.conv2d_out_dims(8, 8, 3, 3, 1, 1, 1, 1, 1, 1)
