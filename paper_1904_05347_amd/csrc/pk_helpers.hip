@@ -7,18 +7,41 @@ namespace pk {
 
 // Fixed-order reduction of split-K partials: C = sum_z ws[z] (+ beta * C).
 // Element e of the M x N result is summed over z = 0, 1, ... in that order,
-// so the result does not depend on scheduling.
+// so the result does not depend on scheduling.  Each work-item owns V
+// consecutive elements of one row (V = 4 when rows and both buffers allow
+// 16-byte accesses) and issues the loads of up to eight partials before the
+// first addition, so a split of S costs about S/8 memory round trips
+// instead of S.
+template <int V>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(const float *ws, float *C, int M, int N,
                                                             int64_t ldc, int splits, float beta)
 {
+    typedef float VT __attribute__((ext_vector_type(V)));
+    constexpr int B = 8;  // partials in flight per work-item
     const int64_t total = (int64_t)M * N;
+    const int nv = N / V;
+    const int64_t items = (int64_t)M * nv;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
-        float s = ws[e];
-        for (int z = 1; z < splits; ++z) s += ws[e + z * total];
-        const int64_t row = e / N, col = e - row * N;
+    for (int64_t it = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; it < items; it += stride) {
+        const int64_t row = it / nv;
+        const int col = (int)(it - row * nv) * V;
+        const float *p = ws + row * N + col;
+        VT s = *reinterpret_cast<const VT *>(p);
+        for (int z = 1; z < splits; z += B) {
+            VT v[B];
+#pragma unroll
+            for (int u = 0; u < B; ++u)
+                if (z + u < splits) v[u] = *reinterpret_cast<const VT *>(p + (int64_t)(z + u) * total);
+#pragma unroll
+            for (int u = 0; u < B; ++u)
+                if (z + u < splits) s += v[u];
+        }
         float *c = C + row * ldc + col;
-        *c = beta != 0.f ? fmaf(beta, *c, s) : s;
+        if (beta != 0.f) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) s[j] = fmaf(beta, c[j], s[j]);
+        }
+        *reinterpret_cast<VT *>(c) = s;
     }
 }
 
@@ -59,10 +82,15 @@ int device_cu_count()
 hipError_t launch_splitk_reduce(const float *ws, float *C, int M, int N, int64_t ldc, int splits,
                                 float beta, hipStream_t stream)
 {
-    const int64_t total = (int64_t)M * N;
-    const int64_t blocks = (total + 255) / 256;
+    const bool v4 = N % 4 == 0 && ldc % 4 == 0 && reinterpret_cast<uintptr_t>(C) % 16 == 0 &&
+                    reinterpret_cast<uintptr_t>(ws) % 16 == 0;
+    const int64_t items = (int64_t)M * N / (v4 ? 4 : 1);
+    const int64_t blocks = (items + 255) / 256;
     const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, stream, ws, C, M, N, ldc, splits, beta);
+    if (v4)
+        hipLaunchKernelGGL(splitk_reduce_kernel<4>, dim3(grid), dim3(256), 0, stream, ws, C, M, N, ldc, splits, beta);
+    else
+        hipLaunchKernelGGL(splitk_reduce_kernel<1>, dim3(grid), dim3(256), 0, stream, ws, C, M, N, ldc, splits, beta);
     return hipGetLastError();
 }
 
