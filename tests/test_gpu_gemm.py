@@ -205,6 +205,40 @@ def test_gemm_workspace_splits_and_streamk():
     assert ran >= 400
 
 
+@pytest.mark.parametrize("cfg,M,N,K,ldc", [
+    ("gemm_64x64x16_w2x2_nn_v11", 37, 27, 900, 29),    # rows of 27: one element per work-item
+    ("gemm_64x64x32_w2x2_nn_v44", 40, 36, 1100, 44)])  # 16-byte elements, padded rows
+def test_split_reduce_widths_and_batches(cfg, M, N, K, ldc):
+    """The split-K reduce on both element widths and with splits that fill
+    its batches of in-flight partials partly (2, 10) and exactly twice (17),
+    into a C whose rows are padded: integer data, bit-exact against the
+    oracle, and the padding columns untouched."""
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(M + N + K)
+    A = wl.integers(rng, M * K).reshape(M, K)
+    B = wl.integers(rng, K * N).reshape(K, N)
+    C = np.full((M, ldc), 7.0, dtype=np.float32)
+    C[:, :N] = wl.integers(rng, M * N).reshape(M, N)
+    ref, _ = oracle.sgemm("N", "N", M, N, K, 1.0, A, K, B, N, 0.5, np.ascontiguousarray(C[:, :N]), N)
+    ws = torch.empty(17 * M * N + 64, dtype=torch.float32, device="cuda")
+    dA, dB = dev(A), dev(B)
+    for splits in (2, 10, 17):
+        dC = dev(C)
+        pk.force_config(cfg)
+        pk.force_splits(splits)
+        try:
+            st = pk.binding.sgemm_ws("N", "N", M, N, K, 1.0, dA.data_ptr(), K, dB.data_ptr(), N, 0.5,
+                                     dC.data_ptr(), ldc, ws.data_ptr(), ws.numel() * 4)
+            used = pk.last_config_name()
+        finally:
+            pk.force_config(None)
+            pk.force_splits(0)
+        assert st == 0 and used == cfg, (cfg, st, used)
+        out = host(dC)
+        assert np.array_equal(out[:, :N].astype(np.float64), ref), (cfg, splits)
+        assert np.all(out[:, N:] == 7.0), (cfg, splits)
+
+
 @pytest.mark.parametrize("M,N,K", [(64, 64, 1024), (1024, 64, 512), (256, 1024, 1024), (100, 36, 2000)])
 def test_gemm_default_workspace(M, N, K):
     """The default choice with the workspace the binding allocates (a split
