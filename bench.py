@@ -576,6 +576,29 @@ def run_ablations(torch, pk, wl):
                       flush=True)
         del dx, df, dy, dA, dB, dC, ws
 
+    # the 4096^2-output GEMM's K loop against its fixed per-call part: the
+    # same configuration at three depths, with and without the read of C
+    rng = np.random.default_rng(4096)
+    dA = torch.from_numpy(wl.uniform(rng, 4096 * 4096).reshape(4096, 4096)).cuda()
+    dB = torch.from_numpy(wl.uniform(rng, 4096 * 4096).reshape(4096, 4096)).cuda()
+    dC = torch.from_numpy(wl.uniform(rng, 4096 * 4096).reshape(4096, 4096)).cuda()
+    cfg = "gemm_256x256x32_w2x4_nn_v44_o2_dma2"
+    for k in (1024, 2048, 4096):
+        Ak, Bk = dA[:, :k].contiguous(), dB[:k].contiguous()
+        for beta in (0.0, 0.5):
+            pk.force_config(cfg)
+            try:
+                med, mn = _time_each(torch, lambda: pk.gemm(Ak, Bk, dC, beta=beta))
+                used = pk.last_config_name()
+            finally:
+                pk.force_config(None)
+            rows.append({"ablation": "K loop vs fixed part", "shape": "gemm NN 4096x4096x%d" % k,
+                         "variant": "beta = %g" % beta, "config": used, "ms_median": round(med, 4),
+                         "ms_min": round(mn, 4), "tflops": round(2.0 * 4096 * 4096 * k / (med * 1e-3) / 1e12, 2)})
+            print("bench: K loop %d beta %g %.4f ms" % (k, beta, med), file=sys.stderr, flush=True)
+        del Ak, Bk
+    del dA, dB, dC
+
     # warm vs cold: a 512 MiB scratch write between calls evicts L2 and MALL
     scratch = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
     for name in ("vgg16 conv1_1 b32 224x224x3->64 3x3", "resnet50 b32 56x56x64->64 1x1",
