@@ -139,8 +139,13 @@ bool gemm_config_fits(const Config *c, int ta, int tb, bool vec_ok)
 // Per-shape tuning table: the fastest compiled configuration (and split of
 // K) measured on MI355X for the shapes the benchmarks run, by timing every
 // compatible configuration with PK_FORCE_CONFIG.  kind: 0 = pk_sgemm,
-// 1 = pk_conv2d_fwd (M = N*Ho*Wo, N = Cout, K = KH*KW*Cin; window and stride
-// complete the key).  splits 0 = the default rule.
+// 1 = pk_conv2d_fwd through the implicit GEMM or the direct kernel, 2 =
+// pk_conv2d_fwd of a 1x1, stride-1, unpadded window, which runs as a plain
+// GEMM on the image (M = N*Ho*Wo, N = Cout, K = KH*KW*Cin; window and stride
+// complete the key).  The two convolution kinds never share an entry: a
+// padded 1x1 window has the M, K, window and stride of an unpadded one but
+// takes the gather path, whose configurations the GEMM path cannot run.
+// splits 0 = the default rule.
 struct TunedShape {
     int kind, ta, tb;
     int64_t M, N, K;
@@ -167,33 +172,33 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 25088, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_2 b32 28x28x512->512 3x3 s1
     {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv5_1 b32 14x14x512->512 3x3 s1
     {1, 0, 0, 401408, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b32 230x230x3->64 7x7 s2
-    {1, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},  // resnet50 conv2_1 b32 56x56x64->256 1x1 s1
+    {2, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},  // resnet50 conv2_1 b32 56x56x64->256 1x1 s1
     // (kept by hand: inside the benchmark step the B-resident and direct-to-LDS
     // forms, faster alone, take 20.0-20.1 us against this one's 19.5)
-    {1, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv2_2 b32 56x56x64->64 1x1 s1
+    {2, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv2_2 b32 56x56x64->64 1x1 s1
     {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // resnet50 conv2_3 b32 56x56x64->64 3x3 s1
-    {1, 0, 0, 100352, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_4 b32 56x56x256->64 1x1 s1
+    {2, 0, 0, 100352, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_4 b32 56x56x256->64 1x1 s1
     {1, 0, 0, 25088, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv2_5 b32 56x56x64->64 3x3 s2
-    {1, 0, 0, 25088, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b32 28x28x64->256 1x1 s1
-    {1, 0, 0, 25088, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_2 b32 28x28x256->512 1x1 s1
-    {1, 0, 0, 25088, 128, 256, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv3_3 b32 28x28x256->128 1x1 s1
+    {2, 0, 0, 25088, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b32 28x28x64->256 1x1 s1
+    {2, 0, 0, 25088, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_2 b32 28x28x256->512 1x1 s1
+    {2, 0, 0, 25088, 128, 256, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv3_3 b32 28x28x256->128 1x1 s1
     {1, 0, 0, 25088, 128, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // resnet50 conv3_4 b32 28x28x128->128 3x3 s1
-    {1, 0, 0, 25088, 512, 128, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv3_5 b32 28x28x128->512 1x1 s1
-    {1, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv3_6 b32 28x28x512->128 1x1 s1
+    {2, 0, 0, 25088, 512, 128, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv3_5 b32 28x28x128->512 1x1 s1
+    {2, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv3_6 b32 28x28x512->128 1x1 s1
     {1, 0, 0, 6272, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv3_7 b32 28x28x128->128 3x3 s2
-    {1, 0, 0, 6272, 512, 128, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv4_1 b32 14x14x128->512 1x1 s1
-    {1, 0, 0, 6272, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_2 b32 14x14x512->1024 1x1 s1
-    {1, 0, 0, 6272, 256, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_3 b32 14x14x512->256 1x1 s1
+    {2, 0, 0, 6272, 512, 128, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv4_1 b32 14x14x128->512 1x1 s1
+    {2, 0, 0, 6272, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_2 b32 14x14x512->1024 1x1 s1
+    {2, 0, 0, 6272, 256, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_3 b32 14x14x512->256 1x1 s1
     {1, 0, 0, 6272, 256, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 3},  // resnet50 conv4_4 b32 14x14x256->256 3x3 s1
-    {1, 0, 0, 6272, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 1},  // resnet50 conv4_5 b32 14x14x256->1024 1x1 s1
-    {1, 0, 0, 6272, 256, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_6 b32 14x14x1024->256 1x1 s1
+    {2, 0, 0, 6272, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44", 1},  // resnet50 conv4_5 b32 14x14x256->1024 1x1 s1
+    {2, 0, 0, 6272, 256, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_6 b32 14x14x1024->256 1x1 s1
     {1, 0, 0, 1568, 256, 2304, 3, 2, "conv_128x128x32_w2x4_v44_o2_dma2", 9},  // resnet50 conv4_7 b32 14x14x256->256 3x3 s2
-    {1, 0, 0, 1568, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv5_1 b32 7x7x256->1024 1x1 s1
-    {1, 0, 0, 1568, 2048, 1024, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_2 b32 7x7x1024->2048 1x1 s1
-    {1, 0, 0, 1568, 512, 1024, 1, 1, "gemm_64x64x32_w2x2_k4_nn_v44_d2", 1},  // resnet50 conv5_3 b32 7x7x1024->512 1x1 s1
+    {2, 0, 0, 1568, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv5_1 b32 7x7x256->1024 1x1 s1
+    {2, 0, 0, 1568, 2048, 1024, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_2 b32 7x7x1024->2048 1x1 s1
+    {2, 0, 0, 1568, 512, 1024, 1, 1, "gemm_64x64x32_w2x2_k4_nn_v44_d2", 1},  // resnet50 conv5_3 b32 7x7x1024->512 1x1 s1
     {1, 0, 0, 1568, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv5_4 b32 7x7x512->512 3x3 s1
-    {1, 0, 0, 1568, 2048, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_5 b32 7x7x512->2048 1x1 s1
-    {1, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 6},  // resnet50 conv5_6 b32 7x7x2048->512 1x1 s1
+    {2, 0, 0, 1568, 2048, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_5 b32 7x7x512->2048 1x1 s1
+    {2, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 6},  // resnet50 conv5_6 b32 7x7x2048->512 1x1 s1
     {1, 0, 0, 50176, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b1 224x224x3->64 3x3 s1
     {1, 0, 0, 50176, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // vgg16 conv1_2 b1 224x224x64->64 3x3 s1
     {1, 0, 0, 12544, 128, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv2_1 b1 112x112x64->128 3x3 s1
@@ -212,53 +217,53 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 3136, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 3},  // vgg16 conv4_1 b4 28x28x256->512 3x3 s1
     {1, 0, 0, 3136, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_2 b4 28x28x512->512 3x3 s1
     {1, 0, 0, 12544, 64, 147, 7, 2, "conv_64x64x16_w2x2_v11", 1},  // resnet50 conv1_1 b1 230x230x3->64 7x7 s2
-    {1, 0, 0, 3136, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b1 56x56x64->256 1x1 s1
-    {1, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
+    {2, 0, 0, 3136, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b1 56x56x64->256 1x1 s1
+    {2, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
     {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 3},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
-    {1, 0, 0, 3136, 64, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
+    {2, 0, 0, 3136, 64, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
     {1, 0, 0, 784, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 8},  // resnet50 conv2_5 b1 56x56x64->64 3x3 s2
-    {1, 0, 0, 784, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b1 28x28x64->256 1x1 s1
-    {1, 0, 0, 784, 512, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
-    {1, 0, 0, 784, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
+    {2, 0, 0, 784, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b1 28x28x64->256 1x1 s1
+    {2, 0, 0, 784, 512, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
+    {2, 0, 0, 784, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
     {1, 0, 0, 784, 128, 1152, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 6},  // resnet50 conv3_4 b1 28x28x128->128 3x3 s1
-    {1, 0, 0, 784, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv3_5 b1 28x28x128->512 1x1 s1
-    {1, 0, 0, 784, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv3_6 b1 28x28x512->128 1x1 s1
+    {2, 0, 0, 784, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv3_5 b1 28x28x128->512 1x1 s1
+    {2, 0, 0, 784, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv3_6 b1 28x28x512->128 1x1 s1
     {1, 0, 0, 196, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv3_7 b1 28x28x128->128 3x3 s2
-    {1, 0, 0, 196, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv4_1 b1 14x14x128->512 1x1 s1
-    {1, 0, 0, 196, 1024, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
-    {1, 0, 0, 196, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
+    {2, 0, 0, 196, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv4_1 b1 14x14x128->512 1x1 s1
+    {2, 0, 0, 196, 1024, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
+    {2, 0, 0, 196, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
     {1, 0, 0, 196, 256, 2304, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 12},  // resnet50 conv4_4 b1 14x14x256->256 3x3 s1
-    {1, 0, 0, 196, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
-    {1, 0, 0, 196, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
+    {2, 0, 0, 196, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
+    {2, 0, 0, 196, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
     {1, 0, 0, 49, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv4_7 b1 14x14x256->256 3x3 s2
-    {1, 0, 0, 49, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
-    {1, 0, 0, 49, 2048, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 8},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
-    {1, 0, 0, 49, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 8},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
+    {2, 0, 0, 49, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
+    {2, 0, 0, 49, 2048, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 8},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
+    {2, 0, 0, 49, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 8},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
     {1, 0, 0, 49, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv5_4 b1 7x7x512->512 3x3 s1
-    {1, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
-    {1, 0, 0, 49, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 8},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
+    {2, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
+    {2, 0, 0, 49, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 8},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
     {1, 0, 0, 50176, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b4 230x230x3->64 7x7 s2
-    {1, 0, 0, 12544, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b4 56x56x64->256 1x1 s1
-    {1, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
+    {2, 0, 0, 12544, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b4 56x56x64->256 1x1 s1
+    {2, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
     {1, 0, 0, 12544, 64, 576, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 1},  // resnet50 conv2_3 b4 56x56x64->64 3x3 s1
-    {1, 0, 0, 12544, 64, 256, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv2_4 b4 56x56x256->64 1x1 s1
+    {2, 0, 0, 12544, 64, 256, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv2_4 b4 56x56x256->64 1x1 s1
     {1, 0, 0, 3136, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 3},  // resnet50 conv2_5 b4 56x56x64->64 3x3 s2
-    {1, 0, 0, 3136, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_2 b4 28x28x256->512 1x1 s1
-    {1, 0, 0, 3136, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_3 b4 28x28x256->128 1x1 s1
+    {2, 0, 0, 3136, 512, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_2 b4 28x28x256->512 1x1 s1
+    {2, 0, 0, 3136, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_3 b4 28x28x256->128 1x1 s1
     {1, 0, 0, 3136, 128, 1152, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 2},  // resnet50 conv3_4 b4 28x28x128->128 3x3 s1
-    {1, 0, 0, 3136, 512, 128, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_5 b4 28x28x128->512 1x1 s1
-    {1, 0, 0, 3136, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma2", 1},  // resnet50 conv3_6 b4 28x28x512->128 1x1 s1
+    {2, 0, 0, 3136, 512, 128, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_5 b4 28x28x128->512 1x1 s1
+    {2, 0, 0, 3136, 128, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma2", 1},  // resnet50 conv3_6 b4 28x28x512->128 1x1 s1
     {1, 0, 0, 784, 128, 1152, 3, 2, "conv_64x64x32_w2x2_k2_v44_dma3", 6},  // resnet50 conv3_7 b4 28x28x128->128 3x3 s2
-    {1, 0, 0, 784, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv4_2 b4 14x14x512->1024 1x1 s1
-    {1, 0, 0, 784, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_3 b4 14x14x512->256 1x1 s1
+    {2, 0, 0, 784, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv4_2 b4 14x14x512->1024 1x1 s1
+    {2, 0, 0, 784, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_3 b4 14x14x512->256 1x1 s1
     {1, 0, 0, 784, 256, 2304, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 4},  // resnet50 conv4_4 b4 14x14x256->256 3x3 s1
-    {1, 0, 0, 784, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv4_5 b4 14x14x256->1024 1x1 s1
-    {1, 0, 0, 784, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 2},  // resnet50 conv4_6 b4 14x14x1024->256 1x1 s1
+    {2, 0, 0, 784, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv4_5 b4 14x14x256->1024 1x1 s1
+    {2, 0, 0, 784, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 2},  // resnet50 conv4_6 b4 14x14x1024->256 1x1 s1
     {1, 0, 0, 196, 256, 2304, 3, 2, "conv_64x64x32_w2x2_k2_v44_dma3", 12},  // resnet50 conv4_7 b4 14x14x256->256 3x3 s2
-    {1, 0, 0, 196, 2048, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma2", 1},  // resnet50 conv5_2 b4 7x7x1024->2048 1x1 s1
-    {1, 0, 0, 196, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv5_3 b4 7x7x1024->512 1x1 s1
-    {1, 0, 0, 196, 2048, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv5_5 b4 7x7x512->2048 1x1 s1
-    {1, 0, 0, 196, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv5_6 b4 7x7x2048->512 1x1 s1
+    {2, 0, 0, 196, 2048, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma2", 1},  // resnet50 conv5_2 b4 7x7x1024->2048 1x1 s1
+    {2, 0, 0, 196, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv5_3 b4 7x7x1024->512 1x1 s1
+    {2, 0, 0, 196, 2048, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv5_5 b4 7x7x512->2048 1x1 s1
+    {2, 0, 0, 196, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv5_6 b4 7x7x2048->512 1x1 s1
     // ResNet-50 56x56x256 1x1 stride 2 -> 128 at batch 32 (the benchmark step's
     // reading of that layer; not a row of the paper's table)
     {1, 0, 0, 25088, 128, 256, 1, 2, "conv_128x128x32_w2x4_v44_o2_dma3", 1},
@@ -277,6 +282,9 @@ bool same_key(const TunedShape &t, int kind, int ta, int tb, int64_t M, int64_t 
     return t.kind == kind && t.ta == ta && t.tb == tb && t.M == M && t.N == N && t.K == K &&
            (kind == 0 || (t.kh == kh && t.stride == stride));
 }
+
+// The tuning table's kind of a convolution (see TunedShape).
+int conv_kind(bool gemm_path) { return gemm_path ? 2 : 1; }
 
 // The tuned configuration for this key, if any: *out is a copy.
 bool find_tuned(int kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t kh, int64_t stride,
@@ -843,10 +851,16 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
     const TunedShape *tuned = nullptr;
     TunedShape tbuf;
     if (!c) {
-        tuned = (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
+        tuned = (KH == KW && sh == sw && find_tuned(conv_kind(gemm_path), 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf
+                                                                                                         : nullptr;
         const bool direct_ok = !gemm_path && pk::direct_conv_fits(nullptr, W, Wo, Cout, KH, KW, Cin, sh, sw) && N <= 65535;
         if (direct_ok && !(tuned && v4)) return 0;
         c = (tuned && v4) ? find_config(tuned->config) : nullptr;
+        // a table entry of the other path (never recorded, but checked) is ignored
+        if (c && (gemm_path ? !gemm_config_fits(c, 0, 0, v4) : !conv_config_fits(c, true, true))) {
+            c = nullptr;
+            tuned = nullptr;
+        }
         if (!c)
             c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cin, Cout, Cout, v4)
                           : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0,
@@ -929,7 +943,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
     const bool gemm_path = KH == 1 && KW == 1 && sh == 1 && sw == 1 && pt == 0 && pl == 0 && pb == 0 && pr == 0;
     TunedShape tbuf;
     const TunedShape *tuned =
-        (KH == KW && sh == sw && find_tuned(1, 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
+        (KH == KW && sh == sw && find_tuned(conv_kind(gemm_path), 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf : nullptr;
     // 1x1, stride 1, no padding: the image is already the M x Cin matrix
     const bool vec_ok = gemm_path && gemm_vec_ok(0, 0, M, Cout, Cin, x, Cin, f, Cout);
     const bool va4 = Cin % 4 == 0 && aligned16(x);
@@ -940,7 +954,8 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
                 return PK_ERR_NOT_SUPPORTED;
         } else {
             c = (tuned && vec_ok) ? find_config(tuned->config) : nullptr;
-            if (c && (!bres_fits(c, Cout, Cin, Cout) || !dma_fits(c, Cin, Cout))) c = nullptr;
+            if (c && (!gemm_config_fits(c, 0, 0, vec_ok) || !bres_fits(c, Cout, Cin, Cout) || !dma_fits(c, Cin, Cout)))
+                c = nullptr;
             if (!c) c = select_gemm(0, 0, M, Cout, Cin, Cin, Cout, Cout, vec_ok);
             // a forced split needs a form that splits K across work-groups
             if (c && t_forced_splits > 1 && c->bres)
@@ -1436,7 +1451,8 @@ int pk_tune_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t 
         }
     }
     if (!best) return PK_ERR_NOT_SUPPORTED;
-    if (!record_tuned({1, 0, 0, M, Cout, K, (int)KH, (int)sh, best->name, best_splits})) return PK_ERR_NOT_SUPPORTED;
+    if (!record_tuned({conv_kind(gemm_path), 0, 0, M, Cout, K, (int)KH, (int)sh, best->name, best_splits}))
+        return PK_ERR_NOT_SUPPORTED;
     fill_result(result, best, best_splits, best_ms, timed);
     t_last_param = 0;
     t_last_config = best->name;

@@ -76,3 +76,33 @@ def test_tune_conv_window_key_and_empty():
     f3 = torch.rand((3, 3, 8, 8), device="cuda")
     assert pk.tune_conv2d(x0, f3)["config"] == ""
     pk.tune_reset()
+
+
+def test_tuned_padded_1x1_does_not_reach_the_gemm_path():
+    """A padded 1x1 window has the (M, K, window, stride) of an unpadded one
+    but runs through the gather; the unpadded one runs as a plain GEMM.  The
+    search's record for the first must never be taken by the second: each
+    keeps a configuration of its own path, with oracle parity."""
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(303)
+    Cin = Cout = 64
+    xp = wl.uniform(rng, 54 * 54 * Cin).reshape(1, 54, 54, Cin)    # pad 1 -> 56 x 56 outputs
+    xu = wl.uniform(rng, 56 * 56 * Cin).reshape(1, 56, 56, Cin)    # no pad -> 56 x 56 outputs
+    f = wl.uniform(rng, Cin * Cout).reshape(1, 1, Cin, Cout)
+    dxp, dxu, df = dev(xp), dev(xu), dev(f)
+    names = {c["name"]: c for c in pk.configs()}
+    try:
+        r = pk.tune_conv2d(dxp, df, padding=(1, 1, 1, 1), iters=2)
+        assert names[r["config"]]["kind"] in (1, 2)   # a gather (or direct) configuration
+        yp = pk.conv2d_fwd(dxp, df, padding=(1, 1, 1, 1))
+        assert pk.last_config_name() == r["config"]
+        ref, scale = oracle.conv2d(xp, f, (1, 1), (1, 1, 1, 1))
+        assert_parity(host(yp), ref, scale, "tuned padded 1x1 " + r["config"])
+        yu = pk.conv2d_fwd(dxu, df, padding=(0, 0, 0, 0))
+        used = pk.last_config_name()
+        assert used.startswith("gemm_") and names[used]["kind"] == 0, used
+        ref, scale = oracle.conv2d(xu, f, (1, 1), (0, 0, 0, 0))
+        assert_parity(host(yu), ref, scale, "unpadded 1x1 after tuning the padded one " + used)
+        assert pk.conv2d_workspace_bytes(1, 56, 56, Cin, 1, 1, Cout, 1, 1, 0, 0, 0, 0) >= 0
+    finally:
+        pk.tune_reset()
