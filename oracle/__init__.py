@@ -7,7 +7,7 @@ TEST INFRASTRUCTURE ONLY: the product package never imports this module.  Only
 The arithmetic lives in ``oracle.c`` (plain C, fp64 accumulation, one output
 element at a time -- the GEMM definition of Section 3.1, the convolution of
 Algorithm 1 with the centred window of Section 4.1, and the Winograd F(2x2, 3x3)
-steps of Section 4.1.2 with their absolute-value error scale).  This module only builds
+and F(4x4, 3x3) steps of Section 4.1.2 with their absolute-value error scale).  This module only builds
 that file with gcc, marshals numpy arrays into it and applies the acceptance
 rule ``|result - ref| <= rtol * scale`` where ``scale = sum_k |a_ik * b_kj|``.
 """
@@ -59,8 +59,9 @@ def _bind(path):
     lib.oracle_conv2d.argtypes = conv_geom + [_p, _p]
     lib.oracle_conv2d_at.argtypes = conv_geom + [_i64, _p, _p, _p]
     wino_geom = [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64, _i64, _i64, _i64, _i64]
-    lib.oracle_winograd_f2x3.argtypes = wino_geom + [_p, _p]
-    lib.oracle_winograd_f2x3_at.argtypes = wino_geom + [_i64, _p, _p, _p]
+    for m in (2, 4):
+        getattr(lib, "oracle_winograd_f%dx3" % m).argtypes = wino_geom + [_p, _p]
+        getattr(lib, "oracle_winograd_f%dx3_at" % m).argtypes = wino_geom + [_i64, _p, _p, _p]
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_threads.argtypes = [ctypes.c_int]
     return lib
@@ -187,42 +188,58 @@ class Oracle:
         del keep
         return ref, scale
 
-    # ------------------------------------------- Winograd F(2x2, 3x3)
+    # ------------------------------------ Winograd F(2x2, 3x3), F(4x4, 3x3)
 
     def _wino_args(self, x, f, pads):
         f = np.asarray(f)
         if f.ndim != 4 or f.shape[0] != 3 or f.shape[1] != 3:
-            raise ValueError("Winograd F(2x2, 3x3) takes a 3 x 3 x Cin x Cout filter")
+            raise ValueError("Winograd F(m x m, 3x3) takes a 3 x 3 x Cin x Cout filter")
         geom, shape, keep = self._conv_args(x, f, (1, 1), pads)
         # drop KH, KW, sh, sw from the direct-convolution argument list
         wgeom = geom[:6] + [geom[8]] + geom[11:]
         return wgeom, shape, keep
 
-    def winograd_f2x3(self, x, f, pads=(1, 1, 1, 1)):
-        """Whole NHWC output of the F(2x2, 3x3) computation (stride 1).
+    def winograd(self, m, x, f, pads=(1, 1, 1, 1)):
+        """Whole NHWC output of the F(m x m, 3x3) computation (stride 1), m = 2 or 4.
 
         Returns (ref, scale) fp64: ref equals the convolution up to fp64
         rounding; scale is the absolute-value chain that bounds the rounding
         of the transformed computation."""
+        if m not in (2, 4):
+            raise ValueError("output tile m is 2 or 4")
         geom, shape, keep = self._wino_args(x, f, pads)
         ref = np.empty(shape, dtype=np.float64)
         scale = np.empty(shape, dtype=np.float64)
-        st = self._lib.oracle_winograd_f2x3(*geom, _ptr(ref), _ptr(scale))
-        _check(st, "winograd_f2x3")
+        st = getattr(self._lib, "oracle_winograd_f%dx3" % m)(*geom, _ptr(ref), _ptr(scale))
+        _check(st, "winograd_f%dx3" % m)
         del keep
         return ref, scale
 
-    def winograd_f2x3_at(self, x, f, pads, flat_idx):
-        """F(2x2, 3x3) outputs at flat NHWC indices.  Returns (ref, scale) fp64."""
+    def winograd_at(self, m, x, f, pads, flat_idx):
+        """F(m x m, 3x3) outputs at flat NHWC indices.  Returns (ref, scale) fp64."""
+        if m not in (2, 4):
+            raise ValueError("output tile m is 2 or 4")
         geom, _shape, keep = self._wino_args(x, f, pads)
         flat_idx = np.ascontiguousarray(flat_idx, dtype=np.int64)
         ref = np.empty(flat_idx.shape, dtype=np.float64)
         scale = np.empty(flat_idx.shape, dtype=np.float64)
-        st = self._lib.oracle_winograd_f2x3_at(*geom, flat_idx.size, _ptr(flat_idx),
-                                               _ptr(ref), _ptr(scale))
-        _check(st, "winograd_f2x3_at")
+        st = getattr(self._lib, "oracle_winograd_f%dx3_at" % m)(*geom, flat_idx.size, _ptr(flat_idx),
+                                                                _ptr(ref), _ptr(scale))
+        _check(st, "winograd_f%dx3_at" % m)
         del keep
         return ref, scale
+
+    def winograd_f2x3(self, x, f, pads=(1, 1, 1, 1)):
+        return self.winograd(2, x, f, pads)
+
+    def winograd_f2x3_at(self, x, f, pads, flat_idx):
+        return self.winograd_at(2, x, f, pads, flat_idx)
+
+    def winograd_f4x3(self, x, f, pads=(1, 1, 1, 1)):
+        return self.winograd(4, x, f, pads)
+
+    def winograd_f4x3_at(self, x, f, pads, flat_idx):
+        return self.winograd_at(4, x, f, pads, flat_idx)
 
 
 def compile_variant(src_text: str, out_path: str) -> "Oracle":
@@ -286,6 +303,14 @@ def winograd_f2x3(*args, **kw):
 
 def winograd_f2x3_at(*args, **kw):
     return _default().winograd_f2x3_at(*args, **kw)
+
+
+def winograd(*args, **kw):
+    return _default().winograd(*args, **kw)
+
+
+def winograd_at(*args, **kw):
+    return _default().winograd_at(*args, **kw)
 
 
 # ------------------------------------------------------------ acceptance

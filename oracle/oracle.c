@@ -18,8 +18,9 @@
  *     tap (x,y) with filter tap (x,y)).
  * Alongside each value it returns scale = sum |product|, the magnitude against
  * which an fp32 result is judged (|gpu - ref| <= 1e-5 * scale).
- * The Winograd F(2x2, 3x3) steps of Section 4.1.2 follow at the end of the
- * file, with their own scale (the same steps on absolute values).
+ * The Winograd F(2x2, 3x3) and F(4x4, 3x3) steps of Section 4.1.2 follow at
+ * the end of the file, with their own scale (the same steps on absolute
+ * values).
  *
  * Storage is row-major (C order).  For GEMM: A is M x K (lda >= K) when
  * transA is 'N', K x M (lda >= M) when 'T'; B is K x N (ldb >= N) or N x K
@@ -273,40 +274,64 @@ int oracle_conv2d_at(const float *x, int64_t N, int64_t H, int64_t W, int64_t Ci
 }
 
 /* ---------------------------------------------------------------------------
- * Winograd convolution F(2x2, 3x3) (Section 4.1.2, the technique of Lavin and
- * Gray that the paper adopts), for a 3x3 window at stride 1.  Every 2x2 block
- * of outputs (tile th, tw) is computed from the 4x4 input tile d that starts
- * at row 2*th - pt, column 2*tw - pl (zero outside the image), in the
+ * Winograd convolution F(m x m, 3 x 3) (Section 4.1.2, the minimal-filtering
+ * technique of Lavin and Gray that the paper adopts), for a 3x3 window at
+ * stride 1, with output tiles of m x m, m = 2 or 4.  Every m x m block of
+ * outputs (tile th, tw) is computed from the (m+2) x (m+2) input tile d that
+ * starts at row m*th - pt, column m*tw - pl (zero outside the image), in the
  * paper's order of steps:
  *   V = BT d BT^T          input transform, per channel
  *   U = G g G^T            filter transform of the 3x3 filter g, per (ci, co)
- *   M = sum_ci U (.) V     16 independent sums over the channels -- the
+ *   M = sum_ci U (.) V     (m+2)^2 independent sums over the channels -- the
  *                          batched matrix multiply of the description
- *   Y = AT M AT^T          output transform to the 2x2 outputs
- * with the minimal-filtering matrices of F(2, 3)
+ *   Y = AT M AT^T          output transform to the m x m outputs
+ * The matrices are the published ones of Lavin and Gray: for F(2, 3) the
+ * interpolation points 0, 1, -1 and infinity,
  *   BT = [1 0 -1 0; 0 1 1 0; 0 -1 1 0; 0 1 0 -1],
  *   G  = [1 0 0; 1/2 1/2 1/2; 1/2 -1/2 1/2; 0 0 1],
- *   AT = [1 1 1 0; 0 1 -1 -1].
+ *   AT = [1 1 1 0; 0 1 -1 -1];
+ * for F(4, 3) the points 0, 1, -1, 2, -2 and infinity (below).  The paper's
+ * trade-off is the tile size: F(4, 3) needs 36 products per 16 outputs per
+ * channel pair against F(2, 3)'s 16 per 4, at the price of larger transform
+ * coefficients (more rounding) and smaller batched products.
  * In exact arithmetic Y is the convolution.  The scale returned with each
  * output is the same chain with every matrix entry and operand replaced by
  * its absolute value: the magnitude that bounds the rounding error of the
  * transformed computation, as sum |a*b| does for the direct sum.
  * ------------------------------------------------------------------------- */
-static const double WG_BT[4][4] = {{1, 0, -1, 0}, {0, 1, 1, 0}, {0, -1, 1, 0}, {0, 1, 0, -1}};
-static const double WG_G[4][3] = {{1, 0, 0}, {0.5, 0.5, 0.5}, {0.5, -0.5, 0.5}, {0, 0, 1}};
-static const double WG_AT[2][4] = {{1, 1, 1, 0}, {0, 1, -1, -1}};
+typedef struct {
+    int m;            /* outputs per tile side; the input tile is m + 2 */
+    double BT[6][6];  /* (m+2) x (m+2) input transform */
+    double G[6][3];   /* (m+2) x 3 filter transform */
+    double AT[4][6];  /* m x (m+2) output transform */
+} wino_matrices;
 
-static void winograd_element(const conv_problem *p, int64_t n, int64_t ho, int64_t wo,
-                             int64_t co, double *ref, double *scale)
+static const wino_matrices WINO_F2 = {
+    2,
+    {{1, 0, -1, 0}, {0, 1, 1, 0}, {0, -1, 1, 0}, {0, 1, 0, -1}},
+    {{1, 0, 0}, {0.5, 0.5, 0.5}, {0.5, -0.5, 0.5}, {0, 0, 1}},
+    {{1, 1, 1, 0}, {0, 1, -1, -1}}};
+
+static const wino_matrices WINO_F4 = {
+    4,
+    {{4, 0, -5, 0, 1, 0}, {0, -4, -4, 1, 1, 0}, {0, 4, -4, -1, 1, 0},
+     {0, -2, -1, 2, 1, 0}, {0, 2, -1, -2, 1, 0}, {0, 4, 0, -5, 0, 1}},
+    {{1.0 / 4, 0, 0}, {-1.0 / 6, -1.0 / 6, -1.0 / 6}, {-1.0 / 6, 1.0 / 6, -1.0 / 6},
+     {1.0 / 24, 1.0 / 12, 1.0 / 6}, {1.0 / 24, -1.0 / 12, 1.0 / 6}, {0, 0, 1}},
+    {{1, 1, 1, 1, 1, 0}, {0, 1, -1, 2, -2, 0}, {0, 1, 1, 4, 4, 0}, {0, 1, -1, 8, -8, 1}}};
+
+static void winograd_element(const conv_problem *p, const wino_matrices *w, int64_t n,
+                             int64_t ho, int64_t wo, int64_t co, double *ref, double *scale)
 {
-    const int64_t th = ho / 2, tw = wo / 2;
-    const int i = (int)(ho % 2), j = (int)(wo % 2);
-    const int64_t ih0 = 2 * th - p->pt, iw0 = 2 * tw - p->pl;
-    double m[4][4] = {{0}}, ma[4][4] = {{0}};
+    const int m = w->m, t = m + 2;
+    const int64_t th = ho / m, tw = wo / m;
+    const int i = (int)(ho % m), j = (int)(wo % m);
+    const int64_t ih0 = m * th - p->pt, iw0 = m * tw - p->pl;
+    double acc[6][6] = {{0}}, acc_abs[6][6] = {{0}};
     for (int64_t ch = 0; ch < p->C; ++ch) {
-        double d[4][4], g[3][3];
-        for (int r = 0; r < 4; ++r)
-            for (int c = 0; c < 4; ++c) {
+        double d[6][6], g[3][3];
+        for (int r = 0; r < t; ++r)
+            for (int c = 0; c < t; ++c) {
                 int64_t ih = ih0 + r, iw = iw0 + c;
                 const int in_image = (ih >= 0 && ih < p->H) && (iw >= 0 && iw < p->W);
                 d[r][c] = in_image ? (double)p->x[((n * p->H + ih) * p->W + iw) * p->C + ch] : 0.0;
@@ -314,28 +339,28 @@ static void winograd_element(const conv_problem *p, int64_t n, int64_t ho, int64
         for (int r = 0; r < 3; ++r)
             for (int c = 0; c < 3; ++c)
                 g[r][c] = (double)p->f[((r * 3 + c) * p->C + ch) * p->K + co];
-        for (int a = 0; a < 4; ++a)
-            for (int b = 0; b < 4; ++b) {
+        for (int a = 0; a < t; ++a)
+            for (int b = 0; b < t; ++b) {
                 double v = 0.0, va = 0.0, u = 0.0, ua = 0.0;
-                for (int r = 0; r < 4; ++r)
-                    for (int c = 0; c < 4; ++c) {
-                        v += WG_BT[a][r] * d[r][c] * WG_BT[b][c];
-                        va += fabs(WG_BT[a][r]) * fabs(d[r][c]) * fabs(WG_BT[b][c]);
+                for (int r = 0; r < t; ++r)
+                    for (int c = 0; c < t; ++c) {
+                        v += w->BT[a][r] * d[r][c] * w->BT[b][c];
+                        va += fabs(w->BT[a][r]) * fabs(d[r][c]) * fabs(w->BT[b][c]);
                     }
                 for (int r = 0; r < 3; ++r)
                     for (int c = 0; c < 3; ++c) {
-                        u += WG_G[a][r] * g[r][c] * WG_G[b][c];
-                        ua += fabs(WG_G[a][r]) * fabs(g[r][c]) * fabs(WG_G[b][c]);
+                        u += w->G[a][r] * g[r][c] * w->G[b][c];
+                        ua += fabs(w->G[a][r]) * fabs(g[r][c]) * fabs(w->G[b][c]);
                     }
-                m[a][b] += u * v;
-                ma[a][b] += ua * va;
+                acc[a][b] += u * v;
+                acc_abs[a][b] += ua * va;
             }
     }
     double y = 0.0, ya = 0.0;
-    for (int a = 0; a < 4; ++a)
-        for (int b = 0; b < 4; ++b) {
-            y += WG_AT[i][a] * m[a][b] * WG_AT[j][b];
-            ya += fabs(WG_AT[i][a]) * ma[a][b] * fabs(WG_AT[j][b]);
+    for (int a = 0; a < t; ++a)
+        for (int b = 0; b < t; ++b) {
+            y += w->AT[i][a] * acc[a][b] * w->AT[j][b];
+            ya += fabs(w->AT[i][a]) * acc_abs[a][b] * fabs(w->AT[j][b]);
         }
     *ref = y;
     *scale = ya;
@@ -348,10 +373,10 @@ static int winograd_setup(conv_problem *p, const float *x, int64_t N, int64_t H,
     return conv_setup(p, x, N, H, W, Cin, f, 3, 3, Cout, 1, 1, pt, pl, pb, pr, Ho, Wo);
 }
 
-/* Whole output of the F(2x2, 3x3) computation: ref and scale are N x Ho x Wo x Cout. */
-int oracle_winograd_f2x3(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
-                         const float *f, int64_t Cout, int64_t pt, int64_t pl, int64_t pb,
-                         int64_t pr, int64_t Ho, int64_t Wo, double *ref, double *scale)
+static int winograd_whole(const wino_matrices *w, const float *x, int64_t N, int64_t H,
+                          int64_t W, int64_t Cin, const float *f, int64_t Cout, int64_t pt,
+                          int64_t pl, int64_t pb, int64_t pr, int64_t Ho, int64_t Wo,
+                          double *ref, double *scale)
 {
     conv_problem p;
     if (winograd_setup(&p, x, N, H, W, Cin, f, Cout, pt, pl, pb, pr, Ho, Wo)) return ORACLE_BAD_ARG;
@@ -361,16 +386,15 @@ int oracle_winograd_f2x3(const float *x, int64_t N, int64_t H, int64_t W, int64_
             for (int64_t wo = 0; wo < Wo; ++wo)
                 for (int64_t co = 0; co < Cout; ++co) {
                     int64_t o = ((n * Ho + ho) * Wo + wo) * Cout + co;
-                    winograd_element(&p, n, ho, wo, co, &ref[o], &scale[o]);
+                    winograd_element(&p, w, n, ho, wo, co, &ref[o], &scale[o]);
                 }
     return ORACLE_OK;
 }
 
-/* Selected outputs of the F(2x2, 3x3) computation, by flat NHWC index. */
-int oracle_winograd_f2x3_at(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
-                            const float *f, int64_t Cout, int64_t pt, int64_t pl, int64_t pb,
-                            int64_t pr, int64_t Ho, int64_t Wo, int64_t count,
-                            const int64_t *flat, double *ref, double *scale)
+static int winograd_sampled(const wino_matrices *w, const float *x, int64_t N, int64_t H,
+                            int64_t W, int64_t Cin, const float *f, int64_t Cout, int64_t pt,
+                            int64_t pl, int64_t pb, int64_t pr, int64_t Ho, int64_t Wo,
+                            int64_t count, const int64_t *flat, double *ref, double *scale)
 {
     conv_problem p;
     if (winograd_setup(&p, x, N, H, W, Cin, f, Cout, pt, pl, pb, pr, Ho, Wo)) return ORACLE_BAD_ARG;
@@ -380,10 +404,46 @@ int oracle_winograd_f2x3_at(const float *x, int64_t N, int64_t H, int64_t W, int
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t s = 0; s < count; ++s) {
         int64_t o = flat[s];
-        int64_t co = o % Cout, pix = o / Cout;
-        int64_t wo = pix % Wo, nh = pix / Wo;
-        int64_t ho = nh % Ho, n = nh / Ho;
-        winograd_element(&p, n, ho, wo, co, &ref[s], &scale[s]);
+        int64_t c_out = o % Cout, pixel = o / Cout;
+        int64_t w_out = pixel % Wo, image_row = pixel / Wo;
+        int64_t h_out = image_row % Ho, img = image_row / Ho;
+        winograd_element(&p, w, img, h_out, w_out, c_out, &ref[s], &scale[s]);
     }
     return ORACLE_OK;
+}
+
+/* Whole output of the F(2x2, 3x3) computation: ref and scale are N x Ho x Wo x Cout. */
+int oracle_winograd_f2x3(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                         const float *f, int64_t Cout, int64_t pt, int64_t pl, int64_t pb,
+                         int64_t pr, int64_t Ho, int64_t Wo, double *ref, double *scale)
+{
+    return winograd_whole(&WINO_F2, x, N, H, W, Cin, f, Cout, pt, pl, pb, pr, Ho, Wo, ref, scale);
+}
+
+/* Selected outputs of the F(2x2, 3x3) computation, by flat NHWC index. */
+int oracle_winograd_f2x3_at(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                            const float *f, int64_t Cout, int64_t pt, int64_t pl, int64_t pb,
+                            int64_t pr, int64_t Ho, int64_t Wo, int64_t count,
+                            const int64_t *flat, double *ref, double *scale)
+{
+    return winograd_sampled(&WINO_F2, x, N, H, W, Cin, f, Cout, pt, pl, pb, pr, Ho, Wo, count, flat,
+                            ref, scale);
+}
+
+/* Whole output of the F(4x4, 3x3) computation: ref and scale are N x Ho x Wo x Cout. */
+int oracle_winograd_f4x3(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                         const float *f, int64_t Cout, int64_t pt, int64_t pl, int64_t pb,
+                         int64_t pr, int64_t Ho, int64_t Wo, double *ref, double *scale)
+{
+    return winograd_whole(&WINO_F4, x, N, H, W, Cin, f, Cout, pt, pl, pb, pr, Ho, Wo, ref, scale);
+}
+
+/* Selected outputs of the F(4x4, 3x3) computation, by flat NHWC index. */
+int oracle_winograd_f4x3_at(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                            const float *f, int64_t Cout, int64_t pt, int64_t pl, int64_t pb,
+                            int64_t pr, int64_t Ho, int64_t Wo, int64_t count,
+                            const int64_t *flat, double *ref, double *scale)
+{
+    return winograd_sampled(&WINO_F4, x, N, H, W, Cin, f, Cout, pt, pl, pb, pr, Ho, Wo, count, flat,
+                            ref, scale);
 }

@@ -450,7 +450,104 @@ def pin_winograd_scale(orc):
         assert np.all(tw >= t * (1 - 1e-12)), pads
 
 
+# -------------------------------------------- Winograd F(4x4, 3x3) (Section 4.1.2)
+
+def pin_winograd_f4_brute_force(orc):
+    """The F(4x4, 3x3) computation is the convolution: equal to the exact
+    brute-force result up to fp64 rounding (its filter transform has the
+    non-dyadic entries 1/6, 1/12, 1/24, so equality is within rounding, not
+    exact), with ragged 4x4 tiles and asymmetric padding."""
+    rng = _rng(29)
+    for H, W in [(3, 3), (5, 7), (6, 6), (9, 4), (10, 11)]:
+        for pads in [(0, 0, 0, 0), (1, 1, 1, 1), (2, 0, 1, 2), (0, 2, 2, 1)]:
+            if H + pads[0] + pads[2] < 3 or W + pads[1] + pads[3] < 3:
+                continue
+            x = _grid_uniform(rng, (2, H, W, 3))
+            f = _grid_uniform(rng, (3, 3, 3, 2))
+            exp, _ = brute_conv(x, f, (1, 1), pads)
+            ref, scale = orc.winograd_f4x3(x, f, pads)
+            assert ref.shape == exp.shape, (H, W, pads, ref.shape, exp.shape)
+            err = np.abs(ref - exp)
+            assert np.all(err <= 1e-12 * scale), (H, W, pads, float(np.max(err / scale)))
+
+
+def pin_winograd_f4_scale(orc):
+    """The F(4x4, 3x3) error scale in closed form.  On all-ones data without
+    padding and with whole tiles, the absolute chain factors per dimension:
+    the rows of |BT| sum to 10, 10, 10, 6, 6, 10 and those of |G| to 1/4,
+    1/2, 1/2, 7/24, 7/24, 1, so the products per transform row are
+    h = (5/2, 5, 5, 7/4, 7/4, 10); the rows of |AT| select
+    s = (16, 17, 24, 48) from them, and the output at position (i, j) of
+    its tile has scale Cin * s_i * s_j (value 9 Cin).  On random data the
+    scale bounds the direct sum of |products| from above."""
+    s = np.array([16.0, 17.0, 24.0, 48.0])
+    for C in (1, 3, 8):
+        x = np.ones((1, 10, 6, C), dtype=np.float32)   # 8 x 4 outputs: whole tiles
+        f = np.ones((3, 3, C, 2), dtype=np.float32)
+        ref, scale = orc.winograd_f4x3(x, f, (0, 0, 0, 0))
+        assert ref.shape == (1, 8, 4, 2)
+        assert np.allclose(ref, 9 * C, rtol=1e-13, atol=0), C
+        i = np.arange(8) % 4
+        j = np.arange(4) % 4
+        want = C * np.outer(s[i], s[j])[None, :, :, None]
+        assert np.allclose(scale, np.broadcast_to(want, scale.shape), rtol=1e-13, atol=0), C
+    rng = _rng(31)
+    x = _grid_uniform(rng, (2, 9, 7, 4))
+    f = _grid_uniform(rng, (3, 3, 4, 3))
+    for pads in [(1, 1, 1, 1), (0, 0, 0, 0), (2, 0, 1, 2)]:
+        _, t = orc.conv2d(x, f, (1, 1), pads)
+        _, tw = orc.winograd_f4x3(x, f, pads)
+        assert np.all(tw >= t * (1 - 1e-12)), pads
+
+
+def pin_winograd_tile_sizes_agree(orc):
+    """F(2x2, 3x3) and F(4x4, 3x3) compute the same convolution: on small
+    integers F(2x2) is exact and F(4x4) within its fp64 rounding of it."""
+    rng = _rng(37)
+    x = rng.integers(-8, 9, size=(2, 11, 9, 6)).astype(np.float32)
+    f = rng.integers(-8, 9, size=(3, 3, 6, 5)).astype(np.float32)
+    for pads in [(1, 1, 1, 1), (0, 0, 0, 0), (2, 1, 0, 2)]:
+        r2, _ = orc.winograd_f2x3(x, f, pads)
+        r4, s4 = orc.winograd_f4x3(x, f, pads)
+        assert np.all(np.abs(r4 - r2) <= 1e-12 * s4), pads
+        assert np.array_equal(np.rint(r4), r2), pads
+
+
+# -------------------------------------------- sampled entry points
+
+def pin_sampled_equals_whole(orc):
+    """Each sampled entry point returns, at every requested flat index, the
+    value and scale of the (separately pinned) whole-output function: the
+    flat-index decomposition n, ho, wo, co is checked on outputs with
+    N > 1, Ho != Wo and Cout > 1, and every index is requested."""
+    rng = _rng(41)
+    A = _grid_uniform(rng, (33, 47))
+    B = _grid_uniform(rng, (47, 21))
+    C = _grid_uniform(rng, (33, 21))
+    ref, scale = orc.sgemm("N", "N", 33, 21, 47, 0.7, A, 47, B, 21, 0.3, C, 21)
+    rows, cols = np.divmod(np.arange(33 * 21), 21)
+    r2, s2 = orc.sgemm_at("N", "N", 33, 21, 47, 0.7, A, 47, B, 21, 0.3, C, 21, rows, cols)
+    assert np.array_equal(r2, ref.reshape(-1)) and np.array_equal(s2, scale.reshape(-1))
+    x = _grid_uniform(rng, (2, 9, 8, 5))
+    f = _grid_uniform(rng, (3, 3, 5, 4))
+    ref, scale = orc.conv2d(x, f, (2, 1), (1, 0, 1, 2))
+    flat = rng.permutation(ref.size)
+    r2, s2 = orc.conv2d_at(x, f, (2, 1), (1, 0, 1, 2), flat)
+    assert np.array_equal(r2, ref.reshape(-1)[flat]) and np.array_equal(s2, scale.reshape(-1)[flat])
+    x = _grid_uniform(rng, (3, 11, 6, 4))
+    f = _grid_uniform(rng, (3, 3, 4, 3))
+    for m in (2, 4):
+        ref, scale = orc.winograd(m, x, f, (1, 0, 2, 1))
+        assert ref.shape[1] != ref.shape[2]
+        flat = rng.permutation(ref.size)
+        r2, s2 = orc.winograd_at(m, x, f, (1, 0, 2, 1), flat)
+        assert np.array_equal(r2, ref.reshape(-1)[flat]), m
+        assert np.array_equal(s2, scale.reshape(-1)[flat]), m
+
+
 ALL_PINS = [pin_gemm_brute_force, pin_conv_brute_force, pin_gemm_identity_permutation,
             pin_conv_delta_filters, pin_all_ones_closed_forms, pin_invariants,
             pin_torch_float64, pin_layer_tables, pin_same_padding_property,
-            pin_winograd_brute_force, pin_winograd_integer_exact, pin_winograd_scale]
+            pin_winograd_brute_force, pin_winograd_integer_exact, pin_winograd_scale,
+            pin_winograd_f4_brute_force, pin_winograd_f4_scale, pin_winograd_tile_sizes_agree,
+            pin_sampled_equals_whole]

@@ -31,25 +31,6 @@ def test_invalid_arguments_rejected(orc):
         orc.sgemm_at("N", "N", 4, 4, 4, 1.0, a, 4, a, 4, 0.0, None, 4, [4], [0])
 
 
-def test_sampled_equals_whole(orc):
-    rng = np.random.default_rng(23)
-    from paper_1904_05347_amd import workloads as wl
-    A = wl.uniform(rng, 33 * 47).reshape(33, 47)
-    B = wl.uniform(rng, 47 * 21).reshape(47, 21)
-    C = wl.uniform(rng, 33 * 21).reshape(33, 21)
-    ref, scale = orc.sgemm("N", "N", 33, 21, 47, 0.7, A, 47, B, 21, 0.3, C, 21)
-    rows = rng.integers(0, 33, 50)
-    cols = rng.integers(0, 21, 50)
-    r2, s2 = orc.sgemm_at("N", "N", 33, 21, 47, 0.7, A, 47, B, 21, 0.3, C, 21, rows, cols)
-    assert np.array_equal(r2, ref[rows, cols]) and np.array_equal(s2, scale[rows, cols])
-    x = wl.uniform(rng, 2 * 9 * 8 * 5).reshape(2, 9, 8, 5)
-    f = wl.uniform(rng, 3 * 3 * 5 * 4).reshape(3, 3, 5, 4)
-    ref, scale = orc.conv2d(x, f, (2, 1), (1, 0, 1, 2))
-    flat = rng.integers(0, ref.size, 60)
-    r2, s2 = orc.conv2d_at(x, f, (2, 1), (1, 0, 1, 2), flat)
-    assert np.array_equal(r2, ref.reshape(-1)[flat]) and np.array_equal(s2, scale.reshape(-1)[flat])
-
-
 # ------------------------------------------- the tolerance has teeth (P8)
 
 def _round_significand(x, bits):

@@ -36,13 +36,26 @@ MUTATIONS = {
     "winograd BT row sign": ("{0, -1, 1, 0}, {0, 1, 0, -1}}", "{0, 1, -1, 0}, {0, 1, 0, -1}}"),
     "winograd G half dropped": ("{0.5, -0.5, 0.5}", "{1, -1, 1}"),
     "winograd AT last entry": ("{0, 1, -1, -1}}", "{0, 1, -1, 1}}"),
-    "winograd tile origin uses left pad": ("ih0 = 2 * th - p->pt", "ih0 = 2 * th - p->pl"),
-    "winograd tile stride 1": ("iw0 = 2 * tw - p->pl", "iw0 = tw - p->pl"),
+    "winograd tile origin uses left pad": ("ih0 = m * th - p->pt", "ih0 = m * th - p->pl"),
+    "winograd tile stride 1": ("iw0 = m * tw - p->pl", "iw0 = tw - p->pl"),
     "winograd last channel dropped": ("for (int64_t ch = 0; ch < p->C; ++ch)", "for (int64_t ch = 0; ch + 1 < p->C; ++ch)"),
-    "winograd scale without abs on AT": ("ya += fabs(WG_AT[i][a]) * ma[a][b] * fabs(WG_AT[j][b]);",
-                                          "ya += WG_AT[i][a] * ma[a][b] * WG_AT[j][b];"),
-    "winograd filter scale without abs": ("ua += fabs(WG_G[a][r]) * fabs(g[r][c]) * fabs(WG_G[b][c]);",
-                                          "ua += fabs(WG_G[a][r]) * g[r][c] * fabs(WG_G[b][c]);"),
+    "winograd scale without abs on AT": ("ya += fabs(w->AT[i][a]) * acc_abs[a][b] * fabs(w->AT[j][b]);",
+                                          "ya += w->AT[i][a] * acc_abs[a][b] * w->AT[j][b];"),
+    "winograd filter scale without abs": ("ua += fabs(w->G[a][r]) * fabs(g[r][c]) * fabs(w->G[b][c]);",
+                                          "ua += fabs(w->G[a][r]) * g[r][c] * fabs(w->G[b][c]);"),
+    "winograd F4 BT entry sign": ("{0, -2, -1, 2, 1, 0}", "{0, -2, -1, 2, -1, 0}"),
+    "winograd F4 G sixth sign": ("{-1.0 / 6, 1.0 / 6, -1.0 / 6}", "{-1.0 / 6, -1.0 / 6, -1.0 / 6}"),
+    "winograd F4 G twenty-fourth": ("{1.0 / 24, 1.0 / 12, 1.0 / 6}, {1.0 / 24,", "{1.0 / 12, 1.0 / 12, 1.0 / 6}, {1.0 / 24,"),
+    "winograd F4 AT minus eight": ("{0, 1, -1, 8, -8, 1}", "{0, 1, -1, 8, 8, 1}"),
+    "winograd F4 tile of 2": ("static const wino_matrices WINO_F4 = {\n    4,", "static const wino_matrices WINO_F4 = {\n    2,"),
+    "winograd sampled rows and columns swapped": ("winograd_element(&p, w, img, h_out, w_out, c_out,",
+                                                  "winograd_element(&p, w, img, w_out, h_out, c_out,"),
+    "winograd sampled channel from the pixel": ("int64_t c_out = o % Cout, pixel = o / Cout;",
+                                                "int64_t c_out = (o / Cout) % Cout, pixel = o / Cout;"),
+    "conv sampled rows and columns swapped": ("conv_element(&p, n, ho, wo, co, &ref[s], &scale[s]);",
+                                              "conv_element(&p, n, wo, ho, co, &ref[s], &scale[s]);"),
+    "gemm sampled column for row": ("C, ldc, rows[s], cols[s], &ref[s], &scale[s]);",
+                                    "C, ldc, rows[s], rows[s] % N, &ref[s], &scale[s]);"),
 }
 
 
