@@ -245,25 +245,6 @@ def test_conv_split_k_forced(splits):
         _run(pk, x, f, (1, 1), (1, 1, 1, 1), workspace=ws[: N * H * W * Cout], splits=splits)
 
 
-@pytest.mark.parametrize("case", wl.VGG_LAYERS + wl.RESNET_LAYERS + [wl.RESNET_ALT], ids=lambda c: c.name)
-def test_conv_layers_sampled(case):
-    """Each layer at batch 32, in the launch configuration the benchmark times."""
-    torch, pk = require_gpu()
-    x, f = case.inputs()
-    N, H, W, Cin = case.x_shape
-    KH, KW, _, Cout = case.f_shape
-    wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
-    ws = torch.empty(max(wsb // 4, 1), dtype=torch.float32, device="cuda") if wsb else None
-    out, cfg = _run(pk, x, f, case.stride, case.pads, workspace=ws)
-    Ho, Wo = case.out_hw
-    assert out.shape == (N, Ho, Wo, Cout)
-    idx = sample_conv_outputs(N, Ho, Wo, Cout, 3000, case.seed)
-    ref, scale = oracle.conv2d_at(x, f, case.stride, case.pads, idx)
-    mx = assert_parity(out.reshape(-1)[idx], ref, scale, case.name + " " + cfg)
-    assert mx < 1e-6
-    assert np.all(np.isfinite(out))
-
-
 def test_conv_batch_zero_and_errors():
     torch, pk = require_gpu()
     x = torch.zeros((0, 5, 5, 4), dtype=torch.float32, device="cuda")
@@ -317,27 +298,31 @@ SUITE = [(b, c) for b in (1, 4, 32) for c in wl.layer_suite(b)]
 
 @pytest.mark.parametrize("batch,case", SUITE, ids=[c.name for _, c in SUITE])
 def test_paper_layer_suite(batch, case):
-    """Every distinct VGG-16 / ResNet-50 layer of the paper at batch 1, 4, 32:
-    the whole output where the oracle is quick, else sampled outputs (every
-    border class included)."""
+    """Every distinct VGG-16 / ResNet-50 layer of the paper at batch 1, 4, 32,
+    into a NaN-filled output: the whole output where the oracle is quick,
+    else the corners of every output tile and sampled outputs (every border
+    class included)."""
+    from tests.test_gpu_fullsize import _conv_tile_corners
     torch, pk = require_gpu()
     x, f = case.inputs()
     N, H, W, Cin = case.x_shape
     KH, KW, _, Cout = case.f_shape
-    wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
-    ws = torch.empty(max(wsb // 4, 1), dtype=torch.float32, device="cuda") if wsb else None
-    out, cfg = _run(pk, x, f, case.stride, case.pads, workspace=ws)
     Ho, Wo = oracle.conv2d_out_dims(H, W, KH, KW, *case.stride, *case.pads)
-    assert out.shape == (N, Ho, Wo, Cout)
+    y = torch.full((N, Ho, Wo, Cout), float("nan"), device="cuda")
+    pk.conv2d_fwd(dev(x), dev(f), stride=case.stride, padding=case.pads, out=y)
+    cfg = pk.last_config_name()
+    out = host(y)
+    assert np.all(np.isfinite(out)), cfg
     macs = N * Ho * Wo * Cout * KH * KW * Cin
     if macs <= 4e8:
         ref, scale = oracle.conv2d(x, f, case.stride, case.pads)
         assert_parity(out, ref, scale, case.name + " " + cfg)
     else:
-        idx = sample_conv_outputs(N, Ho, Wo, Cout, 3000, case.seed)
+        info = {c["name"]: c for c in pk.configs()}[cfg]
+        idx = np.concatenate([_conv_tile_corners(info, N, Ho, Wo, Cout),
+                              sample_conv_outputs(N, Ho, Wo, Cout, 1000, case.seed)])
         ref, scale = oracle.conv2d_at(x, f, case.stride, case.pads, idx)
         assert_parity(out.reshape(-1)[idx], ref, scale, case.name + " " + cfg)
-    assert np.all(np.isfinite(out))
 
 
 STREAMK_GEOMS = [
