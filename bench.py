@@ -49,7 +49,7 @@ def parse():
                     help="step: the benchmark step (default); layers: every VGG-16 / ResNet-50 layer of the "
                          "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
                          "the vendor fp32 GEMM beside it; winograd: the 3x3 stride-1 layers through the "
-                         "Winograd F(2x2, 3x3) path beside the default path; ablations: double buffering, "
+                         "Winograd F(2x2, 3x3) and F(4x4, 3x3) paths beside the default path; ablations: double buffering, "
                          "vector width, wave-tile shape, tile size vs CU fill, operand loader, the convolution's "
                          "gather vs a dense operand, warm vs cold caches; tune: "
                          "the automated parameter search against the built-in choices")
@@ -419,9 +419,11 @@ def run_layer_suite(torch, pk, wl):
 
 def run_winograd_suite(torch, pk, wl):
     """Every 3x3 stride-1 layer of the paper's tables at batch 1, 4, 32: the
-    Winograd F(2x2, 3x3) path beside the default (implicit-GEMM) path.
-    TFLOP/s are nominal (the direct sum's 2*N*Ho*Wo*Cout*9*Cin over the time);
-    product_tflops counts the 16 batched products the Winograd path runs."""
+    Winograd path with output tiles of 2 x 2 (F(2x2, 3x3)) and of 4 x 4
+    (F(4x4, 3x3)) beside the default (implicit-GEMM) path.  TFLOP/s are
+    nominal (the direct sum's 2*N*Ho*Wo*Cout*9*Cin over the time);
+    product_tflops counts the (m+2)^2 batched products each Winograd form
+    runs."""
     rows = []
     for batch in (1, 4, 32):
         for case in wl.layer_suite(batch):
@@ -435,24 +437,28 @@ def run_winograd_suite(torch, pk, wl):
             dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
             wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, 3, 3, Cout, 1, 1, *case.pads)
             ws = torch.empty(wsb // 4, dtype=torch.float32, device="cuda") if wsb else None
-            wwb = pk.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, *case.pads)
-            wws = torch.empty(wwb // 4, dtype=torch.float32, device="cuda")
             ms_d = _time_ms_graph(torch, lambda: pk.conv2d_fwd(dx, df, padding=case.pads, out=dy, workspace=ws))
             cfg_d = pk.last_config_name()
-            ms_w = _time_ms_graph(torch, lambda: pk.conv2d_winograd(dx, df, padding=case.pads, out=dy, workspace=wws))
-            cfg_w = pk.last_config_name()
             flops = wl.conv_flops(case, Ho, Wo)
-            tiles = N * ((Ho + 1) // 2) * ((Wo + 1) // 2)
-            prod_flops = 16 * 2 * tiles * Cin * Cout
-            rows.append({"layer": case.name, "config_direct": cfg_d, "config_winograd": cfg_w,
-                         "ms_direct": round(ms_d, 4), "ms_winograd": round(ms_w, 4),
-                         "speedup": round(ms_d / ms_w, 3),
-                         "tflops_direct": round(flops / (ms_d * 1e-3) / 1e12, 2),
-                         "tflops_winograd_nominal": round(flops / (ms_w * 1e-3) / 1e12, 2),
-                         "product_tflops": round(prod_flops / (ms_w * 1e-3) / 1e12, 2)})
-            del dx, df, dy, ws, wws
-            print("bench: %s direct %.4f ms winograd %.4f ms" % (case.name, ms_d, ms_w), file=sys.stderr,
-                  flush=True)
+            row = {"layer": case.name, "config_direct": cfg_d, "ms_direct": round(ms_d, 4),
+                   "tflops_direct": round(flops / (ms_d * 1e-3) / 1e12, 2)}
+            for m in (2, 4):
+                wwb = pk.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, *case.pads, m)
+                wws = torch.empty(wwb // 4, dtype=torch.float32, device="cuda")
+                ms_w = _time_ms_graph(torch, lambda: pk.conv2d_winograd(dx, df, padding=case.pads, out=dy,
+                                                                        workspace=wws, tile=m))
+                tiles = N * ((Ho + m - 1) // m) * ((Wo + m - 1) // m)
+                prod_flops = (m + 2) ** 2 * 2 * tiles * Cin * Cout
+                row.update({"config_f%d" % m: pk.last_config_name(), "ms_f%d" % m: round(ms_w, 4),
+                            "speedup_f%d" % m: round(ms_d / ms_w, 3),
+                            "tflops_nominal_f%d" % m: round(flops / (ms_w * 1e-3) / 1e12, 2),
+                            "product_tflops_f%d" % m: round(prod_flops / (ms_w * 1e-3) / 1e12, 2),
+                            "workspace_mib_f%d" % m: round(wwb / 2 ** 20, 1)})
+                del wws
+            rows.append(row)
+            del dx, df, dy, ws
+            print("bench: %s direct %.4f ms F2 %.4f ms F4 %.4f ms" % (case.name, ms_d, row["ms_f2"], row["ms_f4"]),
+                  file=sys.stderr, flush=True)
     return {"suite": "winograd", "dtype": "f32", "data": "synthetic", "rows": rows}
 
 

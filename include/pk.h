@@ -197,6 +197,32 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
                            void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Winograd convolution F(m x m, 3x3) with the output-tile size m as a
+ * parameter (Section 4.1.2: the tile size trades fewer multiplications for
+ * larger transform coefficients and smaller batched products), m = 2 or 4.
+ * m = 2 is pk_conv2d_winograd_fwd.  m = 4 uses the published Lavin-Gray
+ * F(4, 3) matrices (interpolation points 0, 1, -1, 2, -2 and infinity):
+ * 6 x 6 input tiles, 36 batched products of (T x Cin)(Cin x Cout) with
+ * T = N * ceil(Ho/4) * ceil(Wo/4), 4x fewer multiplications than the
+ * direct sum.  Accuracy: 1e-5 times the transform chain evaluated on
+ * absolute values (larger for m = 4: its matrices have entries up to 8 and
+ * the non-dyadic 1/6, 1/12, 1/24).
+ *
+ * Arguments and error positions are those of pk_conv2d_winograd_fwd with m
+ * inserted at position 19 (m not 2 or 4: PK_ERR_INVALID_VALUE at 19), so
+ * the workspace is argument 20 (misaligned: PK_ERR_INVALID_VALUE at 20).
+ * pk_conv2d_winograd_tile_workspace_bytes returns 0 for an m other than 2, 4.
+ */
+size_t pk_conv2d_winograd_tile_workspace_bytes(int64_t m, int64_t N, int64_t H, int64_t W,
+                                               int64_t Cin, int64_t Cout, int64_t pt,
+                                               int64_t pl, int64_t pb, int64_t pr);
+int pk_conv2d_winograd_tile_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                                const float *f, int64_t KH, int64_t KW, int64_t Cout,
+                                int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb,
+                                int64_t pr, float *y, int64_t Ho, int64_t Wo, int64_t m,
+                                void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Automated parameter search: the measured, per-device choice of a compiled
  * configuration that the paper makes by hand for each of its devices
  * (Section 5) and plans to automate (Section 7).  Every compiled

@@ -305,6 +305,14 @@ def winograd_f2x3_at(*args, **kw):
     return _default().winograd_f2x3_at(*args, **kw)
 
 
+def winograd_f4x3(*args, **kw):
+    return _default().winograd_f4x3(*args, **kw)
+
+
+def winograd_f4x3_at(*args, **kw):
+    return _default().winograd_f4x3_at(*args, **kw)
+
+
 def winograd(*args, **kw):
     return _default().winograd(*args, **kw)
 

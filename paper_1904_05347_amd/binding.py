@@ -72,6 +72,10 @@ SIGNATURES = {
     "pk_conv2d_winograd_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
                                               _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
                                               _p, ctypes.c_size_t, _p]),
+    "pk_conv2d_winograd_tile_workspace_bytes": (ctypes.c_size_t, [_i64] * 10),
+    "pk_conv2d_winograd_tile_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
+                                                   _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
+                                                   _p, ctypes.c_size_t, _p]),
     "pk_tune_sgemm": (ctypes.c_int, [ctypes.c_char, ctypes.c_char, _i64, _i64, _i64, ctypes.c_float, _p, _i64,
                                      _p, _i64, ctypes.c_float, _p, _i64, _p, ctypes.c_size_t, ctypes.c_int, _p,
                                      ctypes.POINTER(TuneResult)]),
@@ -156,8 +160,15 @@ def conv2d_winograd_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr
                                          y, Ho, Wo, workspace, workspace_bytes, stream)
 
 
-def conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr) -> int:
-    return load().pk_conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr)
+def conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr, tile=2) -> int:
+    return load().pk_conv2d_winograd_tile_workspace_bytes(tile, N, H, W, Cin, Cout, pt, pl, pb, pr)
+
+
+def conv2d_winograd_tile_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo, tile,
+                             workspace, workspace_bytes, stream=None) -> int:
+    """pk_conv2d_winograd_tile_fwd on raw device addresses; returns the status code."""
+    return load().pk_conv2d_winograd_tile_fwd(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr,
+                                              y, Ho, Wo, tile, workspace, workspace_bytes, stream)
 
 
 def conv2d_out_dims(H, W, KH, KW, sh, sw, pt, pl, pb, pr):
@@ -371,12 +382,13 @@ def conv2d_fwd(x, w, stride=(1, 1), padding="SAME", out=None, workspace=None):
     return out
 
 
-def conv2d_winograd(x, w, padding="SAME", out=None, workspace=None):
-    """Winograd F(2x2, 3x3) convolution of NHWC x with a 3 x 3 HWIO w, stride 1.
+def conv2d_winograd(x, w, padding="SAME", out=None, workspace=None, tile=2):
+    """Winograd F(tile x tile, 3x3) convolution of NHWC x with a 3 x 3 HWIO w,
+    stride 1; tile (the output-tile size m) is 2 or 4.
 
     Same result as ``conv2d_fwd`` up to fp32 rounding of the transforms.  The
     workspace (float32 device tensor of at least
-    ``conv2d_winograd_workspace_bytes`` bytes) is allocated when None.
+    ``conv2d_winograd_workspace_bytes(..., tile)`` bytes) is allocated when None.
     """
     import torch
     _check_f32_cuda(x, "x")
@@ -397,13 +409,13 @@ def conv2d_winograd(x, w, padding="SAME", out=None, workspace=None):
     if tuple(out.shape) != (N, Ho, Wo, Cout) or not out.is_contiguous():
         raise ValueError("out must be a contiguous %s tensor" % ((N, Ho, Wo, Cout),))
     if workspace is None:
-        need = conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr)
+        need = conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, pt, pl, pb, pr, tile)
         workspace = torch.empty(max(need // 4, 1), dtype=torch.float32, device=x.device)
     _check_f32_cuda(workspace, "workspace")
-    st = conv2d_winograd_raw(x.data_ptr(), N, H, W, Cin, w.data_ptr(), KH, KW, Cout, 1, 1,
-                             pt, pl, pb, pr, out.data_ptr(), Ho, Wo, workspace.data_ptr(),
-                             workspace.numel() * 4, _stream_handle(out))
-    _check(st, "pk_conv2d_winograd_fwd")
+    st = conv2d_winograd_tile_raw(x.data_ptr(), N, H, W, Cin, w.data_ptr(), KH, KW, Cout, 1, 1,
+                                  pt, pl, pb, pr, out.data_ptr(), Ho, Wo, int(tile), workspace.data_ptr(),
+                                  workspace.numel() * 4, _stream_handle(out))
+    _check(st, "pk_conv2d_winograd_tile_fwd")
     return out
 
 

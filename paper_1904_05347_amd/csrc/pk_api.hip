@@ -1070,43 +1070,48 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
 
 namespace {
 
-// Tiles of 2 x 2 outputs and the three workspace regions (256-byte aligned).
+// Tiles of m x m outputs and the three workspace regions (256-byte aligned):
+// U, V and M hold A*A matrices each, A = m + 2.
 struct WinoPlan {
+    int m, A2;
     int64_t Ho, Wo, TH, TW, T;
     size_t off_u, off_v, off_m, bytes;
 };
 
 // false when the sizes overflow the kernels' indexing.
-bool wino_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Cin, int64_t Cout, WinoPlan *w)
+bool wino_plan(int m, int64_t N, int64_t Ho, int64_t Wo, int64_t Cin, int64_t Cout, WinoPlan *w)
 {
+    w->m = m;
+    w->A2 = (m + 2) * (m + 2);
     w->Ho = Ho;
     w->Wo = Wo;
-    w->TH = (Ho + 1) / 2;
-    w->TW = (Wo + 1) / 2;
+    w->TH = ceil_div(Ho, m);
+    w->TW = ceil_div(Wo, m);
     w->T = checked_mul3(N, w->TH, w->TW);
-    const int64_t u = checked_mul3(16, Cin, Cout), v = checked_mul3(16, w->T, Cin), m = checked_mul3(16, w->T, Cout);
-    if (w->T < 0 || u < 0 || v < 0 || m < 0 || w->T > kMaxDim) return false;
+    const int64_t u = checked_mul3(w->A2, Cin, Cout), v = checked_mul3(w->A2, w->T, Cin),
+                  mm = checked_mul3(w->A2, w->T, Cout);
+    if (w->T < 0 || u < 0 || v < 0 || mm < 0 || w->T > kMaxDim) return false;
     // transform grids: one thread per (tile, channel), < 2^31 work-groups of 256
     if (w->T * Cin >= ((int64_t)1 << 38) || w->T * Cout >= ((int64_t)1 << 38) || Cin * Cout >= ((int64_t)1 << 38))
         return false;
     w->off_u = 0;
     w->off_v = align256((size_t)u * sizeof(float));
     w->off_m = w->off_v + align256((size_t)v * sizeof(float));
-    w->bytes = w->off_m + align256((size_t)m * sizeof(float));
+    w->bytes = w->off_m + align256((size_t)mm * sizeof(float));
     return true;
 }
 
 // The batched product's configuration: a forced one (a non-persistent NN
-// GEMM instance), else 64 x 64 tiles.  A sweep of every instance over the
-// 3x3 stride-1 layers of VGG-16 and ResNet-50 at batch 4 and 32 found
-// 64 x 64 the fastest or within 3 % of it on every layer (16 products keep
-// the chip full; the products are short, Cin deep), with K-blocks of 16 up
-// to Cin = 128 and of 32 beyond.
-const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok, bool *bad)
+// GEMM instance), else by the size of the batch of products.  A sweep of
+// every instance over the 3x3 stride-1 layers of VGG-16 and ResNet-50 at
+// batch 4 and 32 found, for F(2x2, 3x3)'s 16 products, 64 x 64 the fastest
+// or within 3 % of it on every layer (the products are short, Cin deep),
+// with K-blocks of 16 up to Cin = 128 and of 32 beyond.
+const Config *select_wino_gemm(int nbatch, int64_t T, int64_t Cout, int64_t Cin, bool vec_ok, bool *bad)
 {
     const Config *c = forced(bad);
     if (*bad) return nullptr;
-    // the 16 products are (T x Cin) (Cin x Cout), lda = Cin, ldb = Cout
+    // the products are (T x Cin) (Cin x Cout), lda = Cin, ldb = Cout
     if (c)
         return (gemm_config_fits(c, 0, 0, vec_ok) && !c->persistent && !c->streamk && !c->bres && dma_fits(c, Cin, Cout))
                    ? c
@@ -1114,37 +1119,36 @@ const Config *select_wino_gemm(int64_t T, int64_t Cout, int64_t Cin, bool vec_ok
     if (!vec_ok) return find_config("gemm_64x64x16_w2x2_nn_v11");
     if (Cin <= 128) return find_config("gemm_64x64x16_w2x2_nn_v44");
     // deeper channels: operands copied straight into LDS; 128 x 128 tiles
-    // once the 16 products hold 4 of them per CU (VGG-16 conv3_2 .. conv4_2
+    // once the products hold 4 of them per CU (VGG-16 conv3_2 .. conv4_2
     // at batch 32: 0.93-0.95x the time of the register-staged 64 x 64 x 32),
     // else 64 x 64 x 32 in three stages (0.93-0.98x)
-    const bool big = 16 * ceil_div(T, 128) * ceil_div(Cout, 128) >= 4 * kCUs;
+    const bool big = nbatch * ceil_div(T, 128) * ceil_div(Cout, 128) >= 4 * kCUs;
     const Config *c2 = find_config(big ? "gemm_128x128x32_w2x4_nn_v44_o2_dma2" : "gemm_64x64x32_w2x2_nn_v44_dma3");
     if (c2 && dma_fits(c2, Cin, Cout)) return c2;
     return find_config("gemm_64x64x32_w2x2_nn_v44");
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t pk_conv2d_winograd_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, int64_t Cout, int64_t pt,
-                                          int64_t pl, int64_t pb, int64_t pr)
+size_t wino_workspace_bytes(int m, int64_t N, int64_t H, int64_t W, int64_t Cin, int64_t Cout, int64_t pt,
+                            int64_t pl, int64_t pb, int64_t pr)
 {
     int64_t Ho = 0, Wo = 0;
-    if (N < 1 || Cin < 1 || Cout < 1 || Cin > kMaxDim || Cout > kMaxDim) return 0;
+    if ((m != 2 && m != 4) || N < 1 || Cin < 1 || Cout < 1 || Cin > kMaxDim || Cout > kMaxDim) return 0;
     const int saved = t_last_param;
     const int st = out_dims(H, W, 3, 3, 1, 1, pt, pl, pb, pr, &Ho, &Wo, 2);
     t_last_param = saved;
     if (st != PK_OK) return 0;
     WinoPlan w;
-    if (!wino_plan(N, Ho, Wo, Cin, Cout, &w)) return 0;
+    if (!wino_plan(m, N, Ho, Wo, Cin, Cout, &w)) return 0;
     return w.bytes;
 }
 
-int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, const float *f, int64_t KH,
-                           int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb,
-                           int64_t pr, float *y, int64_t Ho, int64_t Wo, void *workspace, size_t workspace_bytes,
-                           void *stream)
+// The Winograd convolution with output tiles of m x m.  Argument positions
+// are pk_conv2d_fwd's; m_pos is the position of m (0 when the entry point has
+// none) and ws_pos that of the workspace.
+int wino_fwd(int m, int m_pos, int ws_pos, const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+             const float *f, int64_t KH, int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl,
+             int64_t pb, int64_t pr, float *y, int64_t Ho, int64_t Wo, void *workspace, size_t workspace_bytes,
+             void *stream)
 {
     begin();
     if (N < 0) return invalid(2);
@@ -1171,6 +1175,7 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
     }
     if (Ho != ho) return invalid(17);
     if (Wo != wo) return invalid(18);
+    if (m != 2 && m != 4) return m_pos ? invalid(m_pos) : PK_ERR_NOT_SUPPORTED;
     if (KH != 3 || KW != 3 || sh != 1 || sw != 1) return PK_ERR_NOT_SUPPORTED;
     if (N == 0) return PK_OK;
     if (!x) return invalid(1);
@@ -1181,9 +1186,9 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
         checked_mul3(pixels, Cin, 1) < 0 || checked_mul3(checked_mul3(N, Ho, Wo), Cout, 1) < 0)
         return PK_ERR_NOT_SUPPORTED;
     WinoPlan w;
-    if (!wino_plan(N, Ho, Wo, Cin, Cout, &w)) return PK_ERR_NOT_SUPPORTED;
+    if (!wino_plan(m, N, Ho, Wo, Cin, Cout, &w)) return PK_ERR_NOT_SUPPORTED;
     if (!workspace || workspace_bytes < w.bytes) return PK_ERR_WORKSPACE;
-    if (!aligned16(workspace)) return invalid(19);
+    if (!aligned16(workspace)) return invalid(ws_pos);
 
     uintptr_t x0, x1, f0, f1, y0, y1;
     span(x, pixels, Cin, Cin, &x0, &x1);
@@ -1191,7 +1196,7 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
     span(y, N * Ho * Wo, Cout, Cout, &y0, &y1);
     if (overlap(y0, y1, x0, x1) || overlap(y0, y1, f0, f1)) return invalid(16);
     const uintptr_t w0 = (uintptr_t)workspace, w1 = w0 + w.bytes;
-    if (overlap(w0, w1, x0, x1) || overlap(w0, w1, f0, f1) || overlap(w0, w1, y0, y1)) return invalid(19);
+    if (overlap(w0, w1, x0, x1) || overlap(w0, w1, f0, f1) || overlap(w0, w1, y0, y1)) return invalid(ws_pos);
 
     float *U = (float *)((char *)workspace + w.off_u);
     float *V = (float *)((char *)workspace + w.off_v);
@@ -1199,13 +1204,14 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
     const bool in4 = Cin % 4 == 0 && aligned16(x);
     const bool out4 = Cout % 4 == 0 && aligned16(y);
     bool bad = false;
-    const Config *c = select_wino_gemm(w.T, Cout, Cin, Cin % 4 == 0 && Cout % 4 == 0, &bad);
+    const Config *c = select_wino_gemm(w.A2, w.T, Cout, Cin, Cin % 4 == 0 && Cout % 4 == 0, &bad);
     if (bad) return invalid(0);  // PK_FORCE_CONFIG names no configuration
     if (!c) return PK_ERR_NOT_SUPPORTED;
 
     hipStream_t s = (hipStream_t)stream;
-    if (pk::launch_wino_filter(f, U, Cin, Cout, s) != hipSuccess) return PK_ERR_LAUNCH;
-    if (pk::launch_wino_input(x, V, H, W, Cin, pt, pl, w.TH, w.TW, w.T, in4, s) != hipSuccess) return PK_ERR_LAUNCH;
+    if (pk::launch_wino_filter(m, f, U, Cin, Cout, s) != hipSuccess) return PK_ERR_LAUNCH;
+    if (pk::launch_wino_input(m, x, V, H, W, Cin, pt, pl, w.TH, w.TW, w.T, in4, s) != hipSuccess)
+        return PK_ERR_LAUNCH;
     KernelArgs a;
     memset(&a, 0, sizeof(a));
     a.A = V;
@@ -1216,15 +1222,51 @@ int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int6
     a.ldc = Cout;
     a.alpha = 1.f;
     a.beta = 0.f;
-    a.nbatch = 16;
+    a.nbatch = w.A2;
     a.stride_a = w.T * Cin;
     a.stride_b = Cin * Cout;
     a.stride_c = w.T * Cout;
     fill_common(a, c, w.T, Cout, Cin, 1);
     if (c->launch(a, s) != hipSuccess) return PK_ERR_LAUNCH;
-    if (pk::launch_wino_output(Mm, y, Ho, Wo, Cout, w.TH, w.TW, w.T, out4, s) != hipSuccess) return PK_ERR_LAUNCH;
+    if (pk::launch_wino_output(m, Mm, y, Ho, Wo, Cout, w.TH, w.TW, w.T, out4, s) != hipSuccess) return PK_ERR_LAUNCH;
     t_last_config = c->name;
     return PK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t pk_conv2d_winograd_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, int64_t Cout, int64_t pt,
+                                          int64_t pl, int64_t pb, int64_t pr)
+{
+    return wino_workspace_bytes(2, N, H, W, Cin, Cout, pt, pl, pb, pr);
+}
+
+int pk_conv2d_winograd_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, const float *f, int64_t KH,
+                           int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb,
+                           int64_t pr, float *y, int64_t Ho, int64_t Wo, void *workspace, size_t workspace_bytes,
+                           void *stream)
+{
+    return wino_fwd(2, 0, 19, x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo, workspace,
+                    workspace_bytes, stream);
+}
+
+size_t pk_conv2d_winograd_tile_workspace_bytes(int64_t m, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                                               int64_t Cout, int64_t pt, int64_t pl, int64_t pb, int64_t pr)
+{
+    if (m != 2 && m != 4) return 0;
+    return wino_workspace_bytes((int)m, N, H, W, Cin, Cout, pt, pl, pb, pr);
+}
+
+int pk_conv2d_winograd_tile_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, const float *f,
+                                int64_t KH, int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl,
+                                int64_t pb, int64_t pr, float *y, int64_t Ho, int64_t Wo, int64_t m,
+                                void *workspace, size_t workspace_bytes, void *stream)
+{
+    const int mm = (m == 2 || m == 4) ? (int)m : -1;
+    return wino_fwd(mm, 19, 20, x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo, workspace,
+                    workspace_bytes, stream);
 }
 
 

@@ -57,13 +57,14 @@ hipError_t launch_scale(float *C, int M, int N, int64_t ldc, float beta, hipStre
 // p[0 .. n) = 0 (a kernel, so that it may be captured in a graph).
 hipError_t launch_zero_ints(int *p, int n, hipStream_t stream);
 
-// Winograd F(2x2, 3x3) transforms (pk_winograd.hip).  U: 16 x Cin x Cout,
-// V: 16 x T x Cin, M: 16 x T x Cout, T = N * TH * TW tiles of 2 x 2 outputs.
-// vec4: channel count divisible by 4 and every pointer 16-byte aligned.
-hipError_t launch_wino_filter(const float *f, float *U, int64_t Cin, int64_t Cout, hipStream_t stream);
-hipError_t launch_wino_input(const float *x, float *V, int64_t H, int64_t W, int64_t Cin, int64_t pt, int64_t pl,
-                             int64_t TH, int64_t TW, int64_t T, bool vec4, hipStream_t stream);
-hipError_t launch_wino_output(const float *M, float *y, int64_t Ho, int64_t Wo, int64_t Cout, int64_t TH,
+// Winograd F(m x m, 3x3) transforms, m = 2 or 4 (pk_winograd.hip); A = m + 2.
+// U: A*A x Cin x Cout, V: A*A x T x Cin, M: A*A x T x Cout, T = N * TH * TW
+// tiles of m x m outputs.  vec4: channel count divisible by 4 and every
+// pointer 16-byte aligned.
+hipError_t launch_wino_filter(int m, const float *f, float *U, int64_t Cin, int64_t Cout, hipStream_t stream);
+hipError_t launch_wino_input(int m, const float *x, float *V, int64_t H, int64_t W, int64_t Cin, int64_t pt,
+                             int64_t pl, int64_t TH, int64_t TW, int64_t T, bool vec4, hipStream_t stream);
+hipError_t launch_wino_output(int m, const float *M, float *y, int64_t Ho, int64_t Wo, int64_t Cout, int64_t TH,
                               int64_t TW, int64_t T, bool vec4, hipStream_t stream);
 
 }  // namespace pk

@@ -1,22 +1,31 @@
-// pk_winograd.hip -- the transforms of the Winograd convolution F(2x2, 3x3)
-// (Section 4.1.2: the Lavin-Gray technique the paper adopts), for a 3x3
-// window at stride 1.  The product in the middle is the batched contraction of
-// pk_kernel.hpp (16 independent Cin-deep products); these kernels are the
-// memory-bound steps around it:
+// pk_winograd.hip -- the transforms of the Winograd convolutions F(2x2, 3x3)
+// and F(4x4, 3x3) (Section 4.1.2: the Lavin-Gray minimal-filtering technique
+// the paper adopts, whose output-tile size m is the parameter it trades: a
+// larger tile needs fewer multiplications per output but has larger transform
+// coefficients and smaller batched products), for a 3x3 window at stride 1.
+// The product in the middle is the batched contraction of pk_kernel.hpp
+// ((m+2)^2 independent Cin-deep products); these kernels are the memory-bound
+// steps around it.  With A = m + 2 (the transformed tile's side):
 //
-//   filter:  U[p][ci][co] = (G g G^T)[p],   g = f[.][.][ci][co]        (3x3 -> 4x4)
-//   input:   V[p][t][ci]  = (B^T d B)[p],   d = the 4x4 input tile t   (zero outside)
-//   product: M[p] = V[p] U[p]               (T x Cin) (Cin x Cout), p = 0..15
-//   output:  y(2 x 2 block of tile t, co) = A^T m A,  m[p] = M[p][t][co]
+//   filter:  U[p][ci][co] = (G g G^T)[p],   g = f[.][.][ci][co]        (3x3 -> AxA)
+//   input:   V[p][t][ci]  = (B^T d B)[p],   d = the AxA input tile t   (zero outside)
+//   product: M[p] = V[p] U[p]               (T x Cin) (Cin x Cout), p = 0..A*A-1
+//   output:  y(m x m block of tile t, co) = A^T mm A,  mm[p] = M[p][t][co]
 //
-// with G = [1 0 0; 1/2 1/2 1/2; 1/2 -1/2 1/2; 0 0 1],
-//      B^T = [1 0 -1 0; 0 1 1 0; 0 -1 1 0; 0 1 0 -1],  A^T = [1 1 1 0; 0 1 -1 -1].
-// Tile t = (n, th, tw) covers outputs rows 2th, 2th+1 and columns 2tw, 2tw+1;
-// its input tile starts at row 2th - pt, column 2tw - pl.  p = 4*a + b for
-// row a, column b of the 4x4 transformed tile.
+// F(2, 3), interpolation points 0, 1, -1, infinity:
+//   G = [1 0 0; 1/2 1/2 1/2; 1/2 -1/2 1/2; 0 0 1],
+//   B^T = [1 0 -1 0; 0 1 1 0; 0 -1 1 0; 0 1 0 -1],  A^T = [1 1 1 0; 0 1 -1 -1].
+// F(4, 3), points 0, 1, -1, 2, -2, infinity:
+//   G = [1/4 0 0; -1/6 -1/6 -1/6; -1/6 1/6 -1/6; 1/24 1/12 1/6; 1/24 -1/12 1/6; 0 0 1],
+//   B^T = [4 0 -5 0 1 0; 0 -4 -4 1 1 0; 0 4 -4 -1 1 0; 0 -2 -1 2 1 0; 0 2 -1 -2 1 0;
+//          0 4 0 -5 0 1],
+//   A^T = [1 1 1 1 1 0; 0 1 -1 2 -2 0; 0 1 1 4 4 0; 0 1 -1 8 -8 1].
+// Tile t = (n, th, tw) covers output rows m*th .. m*th+m-1 and columns
+// m*tw .. m*tw+m-1; its input tile starts at row m*th - pt, column
+// m*tw - pl.  p = A*a + b for row a, column b of the transformed tile.
 //
-// Layout (all row-major, in the caller's workspace): U is 16 matrices
-// Cin x Cout, V is 16 matrices T x Cin, M is 16 matrices T x Cout, so the
+// Layout (all row-major, in the caller's workspace): U is A*A matrices
+// Cin x Cout, V is A*A matrices T x Cin, M is A*A matrices T x Cout, so the
 // product is a batch of plain NN GEMMs.  Every transform thread handles one
 // (tile, channel) pair -- VEC consecutive channels when the channel count
 // allows 16-byte access -- so loads and stores are coalesced along the NHWC
@@ -40,37 +49,91 @@ struct VecT<4> {
     typedef float4 type;
 };
 
+template <typename T>
+__device__ __forceinline__ T vzero();
+template <>
+__device__ __forceinline__ float vzero<float>() { return 0.f; }
+template <>
+__device__ __forceinline__ float4 vzero<float4>() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+
 constexpr int WT_THREADS = 256;
 
-// 1-D transforms of four values along one axis (elementwise on vectors).
-template <typename T>
-__device__ __forceinline__ void input_1d(const T &d0, const T &d1, const T &d2, const T &d3, T &e0, T &e1, T &e2,
-                                         T &e3)
-{
-    e0 = d0 - d2;  // rows of B^T
-    e1 = d1 + d2;
-    e2 = d2 - d1;
-    e3 = d1 - d3;
-}
+// The 1-D transforms along one axis of a tile (elementwise on vectors):
+// e = B^T d (input), r = A^T mm (output), u = G g (filter).
+template <int MT>
+struct Wino;
 
-template <typename T>
-__device__ __forceinline__ void output_1d(const T &m0, const T &m1, const T &m2, const T &m3, T &r0, T &r1)
-{
-    r0 = m0 + m1 + m2;  // rows of A^T
-    r1 = m1 - m2 - m3;
-}
+template <>
+struct Wino<2> {
+    static constexpr int A = 4;
+    template <typename T>
+    __device__ static __forceinline__ void input_1d(const T *d, T *e)
+    {
+        e[0] = d[0] - d[2];
+        e[1] = d[1] + d[2];
+        e[2] = d[2] - d[1];
+        e[3] = d[1] - d[3];
+    }
+    template <typename T>
+    __device__ static __forceinline__ void output_1d(const T *mm, T *r)
+    {
+        r[0] = mm[0] + mm[1] + mm[2];
+        r[1] = mm[1] - mm[2] - mm[3];
+    }
+    __device__ static __forceinline__ void filter_1d(const float *g, float *u)
+    {
+        u[0] = g[0];
+        u[1] = 0.5f * (g[0] + g[1] + g[2]);
+        u[2] = 0.5f * (g[0] - g[1] + g[2]);
+        u[3] = g[2];
+    }
+};
 
-__device__ __forceinline__ void filter_1d(float g0, float g1, float g2, float &u0, float &u1, float &u2, float &u3)
-{
-    u0 = g0;  // rows of G
-    u1 = 0.5f * (g0 + g1 + g2);
-    u2 = 0.5f * (g0 - g1 + g2);
-    u3 = g2;
-}
+template <>
+struct Wino<4> {
+    static constexpr int A = 6;
+    template <typename T>
+    __device__ static __forceinline__ void input_1d(const T *d, T *e)
+    {
+        const T a = d[4] - 4.f * d[2];  // shared by rows 1 and 2
+        const T b = d[3] - 4.f * d[1];
+        const T c = d[4] - d[2];         // shared by rows 3 and 4
+        const T s = 2.f * (d[3] - d[1]);
+        e[0] = 4.f * d[0] - 5.f * d[2] + d[4];
+        e[1] = a + b;
+        e[2] = a - b;
+        e[3] = c + s;
+        e[4] = c - s;
+        e[5] = 4.f * d[1] - 5.f * d[3] + d[5];
+    }
+    template <typename T>
+    __device__ static __forceinline__ void output_1d(const T *mm, T *r)
+    {
+        const T p12 = mm[1] + mm[2], m12 = mm[1] - mm[2];
+        const T p34 = mm[3] + mm[4], m34 = mm[3] - mm[4];
+        r[0] = mm[0] + p12 + p34;
+        r[1] = m12 + 2.f * m34;
+        r[2] = p12 + 4.f * p34;
+        r[3] = m12 + 8.f * m34 + mm[5];
+    }
+    __device__ static __forceinline__ void filter_1d(const float *g, float *u)
+    {
+        const float s = g[0] + g[2];
+        u[0] = 0.25f * g[0];
+        u[1] = (-1.f / 6.f) * (s + g[1]);
+        u[2] = (-1.f / 6.f) * (s - g[1]);
+        const float q = (1.f / 24.f) * g[0] + (1.f / 6.f) * g[2];
+        u[3] = q + (1.f / 12.f) * g[1];
+        u[4] = q - (1.f / 12.f) * g[1];
+        u[5] = g[2];
+    }
+};
 
+template <int MT>
 __global__ void __launch_bounds__(WT_THREADS) wino_filter_kernel(const float *__restrict__ f, float *__restrict__ U,
                                                                  int64_t pairs)
 {
+    constexpr int A = Wino<MT>::A;
     const int64_t e = (int64_t)blockIdx.x * WT_THREADS + threadIdx.x;  // ci * Cout + co
     if (e >= pairs) return;
     float g[3][3];
@@ -78,23 +141,29 @@ __global__ void __launch_bounds__(WT_THREADS) wino_filter_kernel(const float *__
     for (int r = 0; r < 3; ++r)
 #pragma unroll
         for (int c = 0; c < 3; ++c) g[r][c] = f[(int64_t)(r * 3 + c) * pairs + e];
-    float t[4][3];  // G g
+    float t[A][3];  // G g
 #pragma unroll
-    for (int c = 0; c < 3; ++c) filter_1d(g[0][c], g[1][c], g[2][c], t[0][c], t[1][c], t[2][c], t[3][c]);
+    for (int c = 0; c < 3; ++c) {
+        float col[3] = {g[0][c], g[1][c], g[2][c]}, out[A];
+        Wino<MT>::filter_1d(col, out);
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-        float u[4];  // (G g) G^T, row a
-        filter_1d(t[a][0], t[a][1], t[a][2], u[0], u[1], u[2], u[3]);
+        for (int a = 0; a < A; ++a) t[a][c] = out[a];
+    }
 #pragma unroll
-        for (int b = 0; b < 4; ++b) U[(int64_t)(4 * a + b) * pairs + e] = u[b];
+    for (int a = 0; a < A; ++a) {
+        float u[A];  // (G g) G^T, row a
+        Wino<MT>::filter_1d(t[a], u);
+#pragma unroll
+        for (int b = 0; b < A; ++b) U[(int64_t)(A * a + b) * pairs + e] = u[b];
     }
 }
 
-template <int VEC>
+template <int MT, int VEC>
 __global__ void __launch_bounds__(WT_THREADS) wino_input_kernel(const float *__restrict__ x, float *__restrict__ V,
                                                                 int H, int W, int Cin, int pt, int pl, int TH,
                                                                 int TW, int64_t T)
 {
+    constexpr int A = Wino<MT>::A;
     typedef typename VecT<VEC>::type vt;
     const int cv = Cin / VEC;
     const int64_t e = (int64_t)blockIdx.x * WT_THREADS + threadIdx.x;  // t * cv + channel vector
@@ -105,43 +174,42 @@ __global__ void __launch_bounds__(WT_THREADS) wino_input_kernel(const float *__r
     const int64_t nt = t / TW;
     const int th = (int)(nt % TH);
     const int64_t n = nt / TH;
-    const int ih0 = 2 * th - pt, iw0 = 2 * tw - pl;
+    const int ih0 = MT * th - pt, iw0 = MT * tw - pl;
     const float *img = x + n * H * (int64_t)W * Cin + ci;
-    vt d[4][4];
+    vt s[A][A];  // B^T d, one input column at a time
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int ih = ih0 + r;
+    for (int c = 0; c < A; ++c) {
+        const int iw = iw0 + c;
+        vt col[A];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int iw = iw0 + c;
-            vt v;
-            if constexpr (VEC == 1)
-                v = 0.f;
-            else
-                v = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int r = 0; r < A; ++r) {
+            const int ih = ih0 + r;
+            vt v = vzero<vt>();
             if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W)
                 v = *(const vt *)(img + ((int64_t)ih * W + iw) * Cin);
-            d[r][c] = v;
+            col[r] = v;
         }
+        vt out[A];
+        Wino<MT>::input_1d(col, out);
+#pragma unroll
+        for (int a = 0; a < A; ++a) s[a][c] = out[a];
     }
-    vt s[4][4];  // B^T d
-#pragma unroll
-    for (int c = 0; c < 4; ++c) input_1d(d[0][c], d[1][c], d[2][c], d[3][c], s[0][c], s[1][c], s[2][c], s[3][c]);
     const int64_t plane = T * Cin;
-    float *out = V + t * Cin + ci;
+    float *dst = V + t * Cin + ci;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-        vt v[4];  // (B^T d) B, row a
-        input_1d(s[a][0], s[a][1], s[a][2], s[a][3], v[0], v[1], v[2], v[3]);
+    for (int a = 0; a < A; ++a) {
+        vt v[A];  // (B^T d) B, row a
+        Wino<MT>::input_1d(s[a], v);
 #pragma unroll
-        for (int b = 0; b < 4; ++b) *(vt *)(out + (int64_t)(4 * a + b) * plane) = v[b];
+        for (int b = 0; b < A; ++b) *(vt *)(dst + (int64_t)(A * a + b) * plane) = v[b];
     }
 }
 
-template <int VEC>
+template <int MT, int VEC>
 __global__ void __launch_bounds__(WT_THREADS) wino_output_kernel(const float *__restrict__ M, float *__restrict__ y,
                                                                  int Ho, int Wo, int Cout, int TH, int TW, int64_t T)
 {
+    constexpr int A = Wino<MT>::A;
     typedef typename VecT<VEC>::type vt;
     const int cv = Cout / VEC;
     const int64_t e = (int64_t)blockIdx.x * WT_THREADS + threadIdx.x;  // t * cv + channel vector
@@ -153,24 +221,26 @@ __global__ void __launch_bounds__(WT_THREADS) wino_output_kernel(const float *__
     const int th = (int)(nt % TH);
     const int64_t n = nt / TH;
     const int64_t plane = T * Cout;
-    const float *in = M + t * Cout + co;
-    vt m[4][4];
+    const float *src = M + t * Cout + co;
+    vt r[MT][A];  // A^T mm, one transformed column at a time
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int b = 0; b < A; ++b) {
+        vt col[A], out[MT];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) m[a][b] = *(const vt *)(in + (int64_t)(4 * a + b) * plane);
-    vt r[2][4];  // A^T m
+        for (int a = 0; a < A; ++a) col[a] = *(const vt *)(src + (int64_t)(A * a + b) * plane);
+        Wino<MT>::output_1d(col, out);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) output_1d(m[0][b], m[1][b], m[2][b], m[3][b], r[0][b], r[1][b]);
+        for (int i = 0; i < MT; ++i) r[i][b] = out[i];
+    }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int ho = 2 * th + i;
+    for (int i = 0; i < MT; ++i) {
+        const int ho = MT * th + i;
         if (ho >= Ho) continue;
-        vt o[2];  // (A^T m) A, row i
-        output_1d(r[i][0], r[i][1], r[i][2], r[i][3], o[0], o[1]);
+        vt o[MT];  // (A^T mm) A, row i
+        Wino<MT>::output_1d(r[i], o);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int wo = 2 * tw + j;
+        for (int j = 0; j < MT; ++j) {
+            const int wo = MT * tw + j;
             if (wo >= Wo) continue;
             *(vt *)(y + ((n * Ho + ho) * (int64_t)Wo + wo) * Cout + co) = o[j];
         }
@@ -181,34 +251,57 @@ unsigned blocks_for(int64_t threads) { return (unsigned)((threads + WT_THREADS -
 
 }  // namespace
 
-hipError_t launch_wino_filter(const float *f, float *U, int64_t Cin, int64_t Cout, hipStream_t stream)
+hipError_t launch_wino_filter(int m, const float *f, float *U, int64_t Cin, int64_t Cout, hipStream_t stream)
 {
     const int64_t pairs = Cin * Cout;
-    hipLaunchKernelGGL(wino_filter_kernel, dim3(blocks_for(pairs)), dim3(WT_THREADS), 0, stream, f, U, pairs);
+    if (m == 4)
+        hipLaunchKernelGGL(wino_filter_kernel<4>, dim3(blocks_for(pairs)), dim3(WT_THREADS), 0, stream, f, U, pairs);
+    else
+        hipLaunchKernelGGL(wino_filter_kernel<2>, dim3(blocks_for(pairs)), dim3(WT_THREADS), 0, stream, f, U, pairs);
     return hipGetLastError();
 }
 
-hipError_t launch_wino_input(const float *x, float *V, int64_t H, int64_t W, int64_t Cin, int64_t pt, int64_t pl,
-                             int64_t TH, int64_t TW, int64_t T, bool vec4, hipStream_t stream)
+template <int MT>
+static void input_launch(const float *x, float *V, int64_t H, int64_t W, int64_t Cin, int64_t pt, int64_t pl,
+                         int64_t TH, int64_t TW, int64_t T, bool vec4, hipStream_t stream)
 {
     if (vec4)
-        hipLaunchKernelGGL(wino_input_kernel<4>, dim3(blocks_for(T * (Cin / 4))), dim3(WT_THREADS), 0, stream, x, V,
-                           (int)H, (int)W, (int)Cin, (int)pt, (int)pl, (int)TH, (int)TW, T);
+        hipLaunchKernelGGL((wino_input_kernel<MT, 4>), dim3(blocks_for(T * (Cin / 4))), dim3(WT_THREADS), 0, stream,
+                           x, V, (int)H, (int)W, (int)Cin, (int)pt, (int)pl, (int)TH, (int)TW, T);
     else
-        hipLaunchKernelGGL(wino_input_kernel<1>, dim3(blocks_for(T * Cin)), dim3(WT_THREADS), 0, stream, x, V,
-                           (int)H, (int)W, (int)Cin, (int)pt, (int)pl, (int)TH, (int)TW, T);
+        hipLaunchKernelGGL((wino_input_kernel<MT, 1>), dim3(blocks_for(T * Cin)), dim3(WT_THREADS), 0, stream, x,
+                           V, (int)H, (int)W, (int)Cin, (int)pt, (int)pl, (int)TH, (int)TW, T);
+}
+
+hipError_t launch_wino_input(int m, const float *x, float *V, int64_t H, int64_t W, int64_t Cin, int64_t pt,
+                             int64_t pl, int64_t TH, int64_t TW, int64_t T, bool vec4, hipStream_t stream)
+{
+    if (m == 4)
+        input_launch<4>(x, V, H, W, Cin, pt, pl, TH, TW, T, vec4, stream);
+    else
+        input_launch<2>(x, V, H, W, Cin, pt, pl, TH, TW, T, vec4, stream);
     return hipGetLastError();
 }
 
-hipError_t launch_wino_output(const float *M, float *y, int64_t Ho, int64_t Wo, int64_t Cout, int64_t TH,
+template <int MT>
+static void output_launch(const float *M, float *y, int64_t Ho, int64_t Wo, int64_t Cout, int64_t TH, int64_t TW,
+                          int64_t T, bool vec4, hipStream_t stream)
+{
+    if (vec4)
+        hipLaunchKernelGGL((wino_output_kernel<MT, 4>), dim3(blocks_for(T * (Cout / 4))), dim3(WT_THREADS), 0,
+                           stream, M, y, (int)Ho, (int)Wo, (int)Cout, (int)TH, (int)TW, T);
+    else
+        hipLaunchKernelGGL((wino_output_kernel<MT, 1>), dim3(blocks_for(T * Cout)), dim3(WT_THREADS), 0, stream, M,
+                           y, (int)Ho, (int)Wo, (int)Cout, (int)TH, (int)TW, T);
+}
+
+hipError_t launch_wino_output(int m, const float *M, float *y, int64_t Ho, int64_t Wo, int64_t Cout, int64_t TH,
                               int64_t TW, int64_t T, bool vec4, hipStream_t stream)
 {
-    if (vec4)
-        hipLaunchKernelGGL(wino_output_kernel<4>, dim3(blocks_for(T * (Cout / 4))), dim3(WT_THREADS), 0, stream, M,
-                           y, (int)Ho, (int)Wo, (int)Cout, (int)TH, (int)TW, T);
+    if (m == 4)
+        output_launch<4>(M, y, Ho, Wo, Cout, TH, TW, T, vec4, stream);
     else
-        hipLaunchKernelGGL(wino_output_kernel<1>, dim3(blocks_for(T * Cout)), dim3(WT_THREADS), 0, stream, M, y,
-                           (int)Ho, (int)Wo, (int)Cout, (int)TH, (int)TW, T);
+        output_launch<2>(M, y, Ho, Wo, Cout, TH, TW, T, vec4, stream);
     return hipGetLastError();
 }
 
