@@ -46,7 +46,9 @@ typedef enum {
     PK_ERR_INVALID_VALUE = 1, /* an argument is out of range; see pk_last_invalid_param() */
     PK_ERR_NOT_SUPPORTED = 2, /* a well-formed request this library does not implement */
     PK_ERR_WORKSPACE = 3,     /* a forced split-K or stream-K configuration lacks workspace */
-    PK_ERR_LAUNCH = 4         /* the HIP runtime refused a kernel launch */
+    PK_ERR_LAUNCH = 4,        /* the HIP runtime refused a kernel launch */
+    PK_ERR_SCRATCH_LIMIT = 5  /* pk_conv2d_fwd_noalloc: the call needs more scratch than the
+                                 library's static buffer holds (PK_NOALLOC_SCRATCH_BYTES) */
 } pk_status;
 
 /*
@@ -164,6 +166,33 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
                   int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb, int64_t pr,
                   float *y, int64_t Ho, int64_t Wo,
                   void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * pk_conv2d_fwd for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * It runs exactly what pk_conv2d_fwd runs when given the workspace that
+ * pk_conv2d_workspace_bytes() asks for (same configuration, split and
+ * results, bit for bit), with that workspace taken from a static device
+ * buffer of PK_NOALLOC_SCRATCH_BYTES that the library holds on every device
+ * it runs on until the process ends.  It calls no hipMalloc, hipFree or
+ * other allocating routine.
+ *
+ * Arguments, layouts, quick returns and argument positions of errors are
+ * those of pk_conv2d_fwd without the workspace pair.  A call whose
+ * workspace would exceed PK_NOALLOC_SCRATCH_BYTES returns
+ * PK_ERR_SCRATCH_LIMIT before any work is queued (pass a workspace to
+ * pk_conv2d_fwd instead).  The first call on a device looks up that device's
+ * copy of the buffer (no allocation, no stream work).
+ * Every call on one device shares that device's buffer: calls that overlap
+ * in time on one device (two streams, two host threads) race on it and must
+ * be serialised by the caller.  The buffer keeps the last call's contents;
+ * each call clears what it needs zeroed with a kernel on `stream`.
+ */
+#define PK_NOALLOC_SCRATCH_BYTES ((size_t)80 << 20)
+int pk_conv2d_fwd_noalloc(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin,
+                          const float *f, int64_t KH, int64_t KW, int64_t Cout,
+                          int64_t sh, int64_t sw, int64_t pt, int64_t pl, int64_t pb, int64_t pr,
+                          float *y, int64_t Ho, int64_t Wo, void *stream);
 
 /*
  * Winograd convolution F(2x2, 3x3) (Section 4.1.2, the transform technique

@@ -68,6 +68,8 @@ SIGNATURES = {
     "pk_conv2d_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
                                      _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
                                      _p, ctypes.c_size_t, _p]),
+    "pk_conv2d_fwd_noalloc": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
+                                             _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64, _p]),
     "pk_conv2d_winograd_workspace_bytes": (ctypes.c_size_t, [_i64] * 9),
     "pk_conv2d_winograd_fwd": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _i64, _i64, _i64,
                                               _i64, _i64, _i64, _i64, _i64, _i64, _p, _i64, _i64,
@@ -151,6 +153,13 @@ def conv2d_fwd_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, 
     """pk_conv2d_fwd on raw device addresses; returns the status code."""
     return load().pk_conv2d_fwd(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr,
                                 y, Ho, Wo, workspace, workspace_bytes, stream)
+
+
+def conv2d_fwd_noalloc_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo,
+                           stream=None) -> int:
+    """pk_conv2d_fwd_noalloc on raw device addresses; returns the status code."""
+    return load().pk_conv2d_fwd_noalloc(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr,
+                                        y, Ho, Wo, stream)
 
 
 def conv2d_winograd_raw(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo,

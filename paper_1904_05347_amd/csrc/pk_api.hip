@@ -582,6 +582,9 @@ const char *pk_status_string(int status)
     case PK_ERR_NOT_SUPPORTED: return "PK_ERR_NOT_SUPPORTED: request not implemented";
     case PK_ERR_WORKSPACE: return "PK_ERR_WORKSPACE: forced split needs more workspace";
     case PK_ERR_LAUNCH: return "PK_ERR_LAUNCH: the HIP runtime refused a launch";
+    case PK_ERR_SCRATCH_LIMIT:
+        return "PK_ERR_SCRATCH_LIMIT: the call needs more workspace than the static scratch holds "
+               "(pass a workspace to pk_conv2d_fwd)";
     default: return "unknown pk status";
     }
 }
@@ -1062,6 +1065,74 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         a.ws = (float *)workspace;
     }
     return launch(c, a, s);
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------ static scratch
+
+namespace {
+
+// The workspace of pk_conv2d_fwd_noalloc: one copy per device, at that
+// device's own address.  On the host `scratch` names a host-side stand-in,
+// not device memory: only the address hipGetSymbolAddress returns for the
+// current device may reach a kernel or a copy.
+__device__ __align__(256) unsigned char scratch[PK_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_dev[kMaxDevices];
+
+// Device address of `stream`'s device's copy of the scratch, looked up once
+// per device with that device current.
+int scratch_for_stream(hipStream_t stream, void **out)
+{
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return PK_ERR_LAUNCH;
+    int dev = cur;
+    if (stream) {
+        hipDevice_t d = 0;
+        if (hipStreamGetDevice(stream, &d) != hipSuccess) return PK_ERR_LAUNCH;
+        dev = (int)d;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return PK_ERR_NOT_SUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        if (dev != cur && hipSetDevice(dev) != hipSuccess) return PK_ERR_LAUNCH;
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (dev != cur) (void)hipSetDevice(cur);
+        if (e != hipSuccess || !p) return PK_ERR_LAUNCH;
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return PK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int pk_conv2d_fwd_noalloc(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, const float *f,
+                          int64_t KH, int64_t KW, int64_t Cout, int64_t sh, int64_t sw, int64_t pt, int64_t pl,
+                          int64_t pb, int64_t pr, float *y, int64_t Ho, int64_t Wo, void *stream)
+{
+    // the workspace pk_conv2d_fwd would be given (0 also for arguments that
+    // pk_conv2d_fwd then rejects with their positions)
+    const size_t need = pk_conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, sh, sw, pt, pl, pb, pr);
+    if (need > PK_NOALLOC_SCRATCH_BYTES) {
+        begin();
+        return PK_ERR_SCRATCH_LIMIT;
+    }
+    void *ws = nullptr;
+    if (need > 0) {
+        const int st = scratch_for_stream((hipStream_t)stream, &ws);
+        if (st != PK_OK) {
+            begin();
+            return st;
+        }
+    }
+    return pk_conv2d_fwd(x, N, H, W, Cin, f, KH, KW, Cout, sh, sw, pt, pl, pb, pr, y, Ho, Wo, ws, need, stream);
 }
 
 }  // extern "C"
