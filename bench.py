@@ -45,17 +45,20 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
     ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep", "winograd", "ablations",
-                                                      "tune"),
+                                                      "tune", "direct"),
                     help="step: the benchmark step (default); layers: every VGG-16 / ResNet-50 layer of the "
                          "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
                          "the vendor fp32 GEMM beside it; winograd: the 3x3 stride-1 layers through the "
                          "Winograd F(2x2, 3x3) and F(4x4, 3x3) paths beside the default path; ablations: double buffering, "
                          "vector width, wave-tile shape, tile size vs CU fill, operand loader, the convolution's "
                          "gather vs a dense operand, warm vs cold caches; tune: "
-                         "the automated parameter search against the built-in choices")
+                         "the automated parameter search against the built-in choices; direct: every tiled "
+                         "direct-convolution instance (tile x channel widths) on the small-channel layers")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
                          "the HBM copy bandwidth and the vendor fp32 GEMM at 4096^3, print one JSON line")
+    ap.add_argument("--text", action="store_true",
+                    help="with --suite direct: print the tile x channel-width table instead of JSON")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, run one device-to-device copy of this many MiB (a kernel of "
                          "known traffic that scales the HBM byte counters)")
@@ -415,6 +418,85 @@ def run_layer_suite(torch, pk, wl):
             del dx, df, dy, ws
             print("bench: %s %.4f ms" % (case.name, ms), file=sys.stderr, flush=True)
     return {"suite": "layers", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
+def run_direct_suite(torch, pk, wl):
+    """The tiled direct convolution's parameter space (Section 4.1.1: output
+    tile x output- and input-channel widths) on the paper's small-channel
+    first layers and a 3x3 layer with 16 input channels, at batch 32 (and the
+    first layers at 1 and 4): every instance that takes the layer, forced,
+    graph-timed, beside the default selection.  Rows carry the tile (rows x
+    columns), the channel widths and TFLOP/s, the data of the heatmap."""
+    layers = [c for c in wl.layer_suite(32) if c.x_shape[3] == 3]
+    layers += [c for b in (1, 4) for c in wl.layer_suite(b) if c.x_shape[3] == 3]
+    layers.append(wl.ConvCase("synthetic b32 56x56x16->64 3x3 s1", 32, 56, 56, 16, 3, 3, 64, (1, 1),
+                              (1, 1, 1, 1), 77, (56, 56)))
+    tiled = [c for c in pk.configs() if c["kind"] == 2]
+    rows = []
+    for case in layers:
+        x, f = case.inputs()
+        N, H, W, Cin = case.x_shape
+        KH, KW, _, Cout = case.f_shape
+        Ho, Wo = pk.conv2d_out_dims(H, W, KH, KW, *case.stride, *case.pads)
+        dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+        dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+        flops = wl.conv_flops(case, Ho, Wo)
+        wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
+        ws = torch.empty(wsb // 4, dtype=torch.float32, device="cuda") if wsb else None
+        ms = _time_ms_graph(torch, lambda: pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads, out=dy,
+                                                         workspace=ws))
+        rows.append({"layer": case.name, "config": pk.last_config_name(), "variant": "default", "ms": round(ms, 4),
+                     "tflops": round(flops / (ms * 1e-3) / 1e12, 2)})
+        for cfg in tiled:
+            pk.force_config(cfg["name"])
+            try:
+                pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads, out=dy)
+            except pk.PkError:
+                pk.force_config(None)
+                continue
+            try:
+                ms = _time_ms_graph(torch, lambda: pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads,
+                                                                 out=dy))
+            finally:
+                pk.force_config(None)
+            rows.append({"layer": case.name, "config": cfg["name"], "variant": "forced", "ms": round(ms, 4), "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+                         "frac_mfma_peak": round(flops / (ms * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4)})
+            print("bench: %s %s %.4f ms" % (case.name, cfg["name"], ms), file=sys.stderr, flush=True)
+        del dx, df, dy, ws
+    return {"suite": "direct", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
+def direct_heatmap(result):
+    """The direct suite as text: per layer, one row per output tile
+    (rows x columns of a work-group) and one column per (output channels,
+    input-channel load width), TFLOP/s in the cells; the default selection
+    and the fixed-tile kernels below."""
+    import re
+    out = []
+    layers = []
+    for r in result["rows"]:
+        if r["layer"] not in layers:
+            layers.append(r["layer"])
+    for layer in layers:
+        rows = [r for r in result["rows"] if r["layer"] == layer]
+        cells, other = {}, []
+        for r in rows:
+            m = re.match(r"direct_(\d+)x(\d+)x(\d+)_v(\d+)$", r["config"])
+            if r["variant"] == "forced" and m:
+                tr, tc, ch, vi = (int(v) for v in m.groups())
+                cells[(tr, tc), (ch, vi)] = r["tflops"]
+            else:
+                other.append("  %s %s: %.4f ms, %.2f TFLOP/s" % (r["variant"], r["config"], r["ms"], r["tflops"]))
+        cols = sorted({c for _, c in cells})
+        tiles = sorted({t for t, _ in cells})
+        out.append(layer)
+        out.append("  %-10s" % "tile" + "".join("  ch%-3d v%d" % c for c in cols))
+        for t in tiles:
+            out.append("  %-10s" % ("%dx%d" % t) +
+                       "".join(("%9.1f" % cells[t, c]) if (t, c) in cells else "%9s" % "-" for c in cols))
+        out.extend(other)
+        out.append("")
+    return "\n".join(out)
 
 
 def run_winograd_suite(torch, pk, wl):
@@ -821,6 +903,10 @@ def main():
         return
     if args.suite == "ablations":
         print(json.dumps(run_ablations(torch, pk, wl)))
+        return
+    if args.suite == "direct":
+        res = run_direct_suite(torch, pk, wl)
+        print(direct_heatmap(res) if args.text else json.dumps(res))
         return
     if args.suite == "tune":
         print(json.dumps(run_tune_suite(torch, pk, wl)))

@@ -967,7 +967,8 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
         }
     } else {
         auto direct_ok = [&](const Config *d) {
-            return N <= 65535 && pk::direct_conv_fits(d, W, Wo, Cout, KH, KW, Cin, sh, sw);
+            return N <= 65535 && pk::direct_conv_fits(d, W, Wo, Cout, KH, KW, Cin, sh, sw) &&
+                   (d->vec_a == 1 || va4);
         };
         // the direct-to-LDS gather addresses the image in 32-bit byte offsets
         const bool dma_ok = (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31);

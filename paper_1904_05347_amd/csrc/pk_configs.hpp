@@ -37,7 +37,17 @@ struct Config {
     int bres;  // 1 = op(B) resident in LDS: runs only products with K == bk and N a multiple of bn
     int kgroups = 1;  // groups of waves splitting K inside the work-group (gemm_ksplit_kernel)
     int dma = 0;      // LDS stages filled straight from global memory (gemm_dma_kernel); 0 = register-staged
+    // tiled direct convolution (pk_direct_tiled.hip): output rows of a
+    // work-group's tile (its columns are bm / tile_rows, its channels bn, its
+    // input-channel load width vec_a); 0 for every other kind
+    int tile_rows = 0;
 };
+
+// LDS a tiled direct convolution instance may ask for at launch (dynamic).
+constexpr int kDirectTiledMaxLds = 65536;
+// Bytes of LDS tiled direct instance c needs for this window (-1 when the
+// sizes are out of range).
+size_t direct_tiled_lds_bytes(const Config *c, int64_t KH, int64_t KW, int64_t Cin, int64_t sh, int64_t sw);
 
 // The registry (defined with the kernel instances, host side only).
 const Config *configs(int *count);
@@ -47,9 +57,9 @@ hipError_t launch_splitk_reduce(const float *ws, float *C, int M, int N, int64_t
 // Compute units of the current device (queried once per device).
 int device_cu_count();
 
-// Whether the tiled direct convolution takes this window (short reduction,
-// input patch fits its LDS buffer): configuration c, or any direct
-// configuration when c is NULL.
+// Whether a direct convolution configuration takes this window: c, or, when
+// c is NULL, the fixed-tile short-reduction kernel that the rules choose
+// (reduction of at most 32, input patch fits its LDS buffer).
 bool direct_conv_fits(const Config *c, int64_t W, int64_t Wo, int64_t Cout, int64_t KH, int64_t KW, int64_t Cin,
                       int64_t sh, int64_t sw);
 

@@ -475,6 +475,15 @@ hipError_t launch_direct(const KernelArgs &a, hipStream_t stream)
 bool direct_conv_fits(const Config *c, int64_t W, int64_t Wo, int64_t Cout, int64_t KH, int64_t KW, int64_t Cin,
                       int64_t sh, int64_t sw)
 {
+    if (c && c->tile_rows > 0) {
+        // the tiled instances: patch and filter block within their LDS, whole
+        // input-channel vectors, grid dimensions in range (the batch is the
+        // caller's check); patch offsets are 32-bit, image and output offsets 64-bit
+        const size_t lds = direct_tiled_lds_bytes(c, KH, KW, Cin, sh, sw);
+        const int64_t tc = c->bm / c->tile_rows;
+        return lds <= (size_t)kDirectTiledMaxLds && Cin % c->vec_a == 0 && (Cout + c->bn - 1) / c->bn <= 65535 &&
+               (Wo + tc - 1) / tc < ((int64_t)1 << 20) && W < ((int64_t)1 << 30);
+    }
     if (KH > DT_KMAX || KW > DT_KMAX || Cin > DT_KMAX || sh > 64 || sw > 64) return false;
     if (KH * KW * Cin > DT_KMAX) return false;
     const int64_t pf = direct_patch_floats(KH, KW, Cin, sh, sw);

@@ -382,3 +382,55 @@ def test_streamk_needs_workspace():
     finally:
         pk.force_config(None)
     assert st == 3
+
+
+TILED_GEOMS = [
+    # (N, H, W, Cin, KH, KW, Cout, stride, pads)
+    (2, 37, 45, 3, 7, 7, 64, (2, 2), (3, 3, 3, 3)),     # ResNet-50's first-layer window, ragged tiles
+    (1, 30, 70, 3, 3, 3, 72, (1, 1), (1, 1, 1, 1)),     # VGG's first-layer window, ragged channel block
+    (2, 19, 21, 16, 3, 3, 40, (1, 1), (1, 1, 1, 1)),    # Cin = 16: 4-wide channel loads, K = 144
+    (1, 12, 9, 5, 5, 3, 7, (2, 1), (2, 0, 1, 2)),       # odd window, odd K, asymmetric padding
+    (3, 8, 8, 4, 1, 1, 33, (2, 2), (0, 0, 0, 0)),       # 1x1 stride 2, K = 4
+]
+
+
+def test_tiled_direct_configs_every_instance():
+    """Every tiled direct-convolution instance (output tile x channel widths
+    of Section 4.1.1) on windows up to 7x7 stride 2, ragged output tiles and
+    channel blocks, odd reductions and asymmetric padding: integer data
+    bit-exact against the oracle into a NaN-filled output, and uniform data
+    within the bound.  An instance that cannot take a window (LDS, channel
+    width) must say so with PK_ERR_NOT_SUPPORTED, never run."""
+    torch, pk = require_gpu()
+    tiled = [c for c in pk.configs() if c["kind"] == 2 and c["name"].endswith(("_v1", "_v4"))]
+    assert len(tiled) >= 20
+    ran = 0
+    for gi, (N, H, W, Cin, KH, KW, Cout, stride, pads) in enumerate(TILED_GEOMS):
+        rng = np.random.default_rng(500 + gi)
+        xi = wl.integers(rng, N * H * W * Cin).reshape(N, H, W, Cin)
+        fi = wl.integers(rng, KH * KW * Cin * Cout).reshape(KH, KW, Cin, Cout)
+        xu = wl.uniform(rng, xi.size).reshape(xi.shape)
+        fu = wl.uniform(rng, fi.size).reshape(fi.shape)
+        ref_i, _ = oracle.conv2d(xi, fi, stride, pads)
+        ref_u, scale_u = oracle.conv2d(xu, fu, stride, pads)
+        dxi, dfi, dxu, dfu = dev(xi), dev(fi), dev(xu), dev(fu)
+        for cfg in tiled:
+            if Cin % cfg["vec_a"]:
+                continue
+            pk.force_config(cfg["name"])
+            try:
+                y = torch.full(ref_i.shape, float("nan"), device="cuda")
+                try:
+                    pk.conv2d_fwd(dxi, dfi, stride=stride, padding=pads, out=y)
+                except pk.PkError as e:
+                    assert e.status == 2, (cfg["name"], gi, e)
+                    continue
+                assert pk.last_config_name() == cfg["name"]
+                out = host(y)
+                assert np.array_equal(out.astype(np.float64), ref_i), (cfg["name"], gi)
+                yu = pk.conv2d_fwd(dxu, dfu, stride=stride, padding=pads)
+                assert_parity(host(yu), ref_u, scale_u, "%s %d" % (cfg["name"], gi))
+                ran += 1
+            finally:
+                pk.force_config(None)
+    assert ran >= 50
