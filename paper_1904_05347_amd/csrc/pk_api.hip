@@ -176,7 +176,7 @@ const TunedShape kTuned[] = {
     // (kept by hand: inside the benchmark step the B-resident and direct-to-LDS
     // forms, faster alone, take 20.0-20.1 us against this one's 19.5)
     {2, 0, 0, 100352, 64, 64, 1, 1, "gemm_64x64x16_w2x2_nn_v44", 1},  // resnet50 conv2_2 b32 56x56x64->64 1x1 s1
-    {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // resnet50 conv2_3 b32 56x56x64->64 3x3 s1
+    {1, 0, 0, 100352, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv2_3 b32 56x56x64->64 3x3 s1
     {2, 0, 0, 100352, 64, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv2_4 b32 56x56x256->64 1x1 s1
     {1, 0, 0, 25088, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv2_5 b32 56x56x64->64 3x3 s2
     {2, 0, 0, 25088, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b32 28x28x64->256 1x1 s1

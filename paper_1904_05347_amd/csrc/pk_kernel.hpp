@@ -37,6 +37,7 @@
 #include <utility>
 
 #include "pk_args.hpp"
+#include "pk_partition.hpp"
 
 namespace pk {
 
@@ -50,13 +51,7 @@ enum AMode { A_KCONTIG = 0, A_MCONTIG = 1, A_CONV = 2 };
 // Tile (tm, tn) of logical tile index t, in column strips of group_m tile-rows.
 __device__ __forceinline__ void tile_of(const KernelArgs &p, int t, int &tm, int &tn)
 {
-    const int group = p.group_m * p.tiles_n;
-    const int gid = t / group;
-    const int first_m = gid * p.group_m;
-    const int gsz = min(p.tiles_m - first_m, p.group_m);
-    const int in_group = t - gid * group;
-    tm = first_m + in_group % gsz;
-    tn = in_group / gsz;
+    tile_of_ints(p.tiles_m, p.tiles_n, p.group_m, t, tm, tn);
 }
 
 // Maps the linear work-group id to a C tile.  Work-groups are handed to the
@@ -66,14 +61,7 @@ __device__ __forceinline__ void tile_of(const KernelArgs &p, int t, int &tm, int
 // group_m tile-rows so that concurrently running tiles reuse panels.
 __device__ __forceinline__ void tile_coords(const KernelArgs &p, int &tm, int &tn)
 {
-    int pid = blockIdx.x;
-    const int num = p.tiles_m * p.tiles_n;
-    if (p.xcds > 1) {
-        const int q = num / p.xcds, r = num % p.xcds;
-        const int x = pid % p.xcds, loc = pid / p.xcds;
-        pid = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + loc;
-    }
-    tile_of(p, pid, tm, tn);
+    tile_of(p, xcd_tile(blockIdx.x, p.tiles_m * p.tiles_n, p.xcds), tm, tn);
 }
 
 template <int V>
@@ -1333,15 +1321,6 @@ gemm_persistent_kernel(KernelArgs p)
 // summing a contiguous run of its K-blocks (the blocked identity over a
 // partition of K, Section 3.1.1).  A work-group's first and last tile may be
 // such partial tiles; their partial sums go to slot 2g and 2g+1.
-struct StreamK {
-    int T, G, nkb;
-
-    __device__ __forceinline__ int start(int g) const { return (int)(((int64_t)g * T) / G); }
-    // the work-group whose range holds iteration i: the largest g with start(g) <= i
-    __device__ __forceinline__ int owner(int i) const { return (int)(((int64_t)(i + 1) * G + T - 1) / T) - 1; }
-    __device__ __forceinline__ int slot(int g, int t) const { return start(g) / nkb == t ? 2 * g : 2 * g + 1; }
-};
-
 // Stream-K form of the persistent contraction.  The grid is the resident
 // work-groups; each runs the one-barrier K pipeline over its iteration range,
 // across tile boundaries.  A tile whose K-blocks all fall in one range is
@@ -1374,8 +1353,7 @@ gemm_streamk_kernel(KernelArgs p)
 
     // work-group b runs on XCD b % xcds: give each XCD a contiguous share of
     // the logical ranges, so the tiles an XCD works on are neighbours
-    int lg = blockIdx.x;
-    if (p.xcds > 1 && sk.G % p.xcds == 0) lg = (blockIdx.x % p.xcds) * (sk.G / p.xcds) + blockIdx.x / p.xcds;
+    const int lg = sk_logical(blockIdx.x, sk.G, p.xcds);
     const int end = sk.start(lg + 1);
     int seg = sk.start(lg);  // first iteration of the current segment
     if (seg >= end) return;  // uniform over the work-group, before any barrier
@@ -1727,8 +1705,7 @@ gemm_dma_streamk_kernel(KernelArgs p)
 
     // work-group b runs on XCD b % xcds: give each XCD a contiguous share of
     // the logical ranges, so the tiles an XCD works on are neighbours
-    int lg = blockIdx.x;
-    if (p.xcds > 1 && sk.G % p.xcds == 0) lg = (blockIdx.x % p.xcds) * (sk.G / p.xcds) + blockIdx.x / p.xcds;
+    const int lg = sk_logical(blockIdx.x, sk.G, p.xcds);
     const int beg = sk.start(lg), end = sk.start(lg + 1);
     if (beg >= end) return;  // uniform over the work-group, before any barrier
 
