@@ -469,7 +469,8 @@ def run_direct_suite(torch, pk, wl):
 def direct_heatmap(result):
     """The direct suite as text: per layer, one row per output tile
     (rows x columns of a work-group) and one column per (output channels,
-    input-channel load width), TFLOP/s in the cells; the default selection
+    input-channel load width v1 / v4, or tp: the persistent form with
+    double-buffered patches), TFLOP/s in the cells; the default selection
     and the fixed-tile kernels below."""
     import re
     out = []
@@ -481,16 +482,16 @@ def direct_heatmap(result):
         rows = [r for r in result["rows"] if r["layer"] == layer]
         cells, other = {}, []
         for r in rows:
-            m = re.match(r"direct_(\d+)x(\d+)x(\d+)_v(\d+)$", r["config"])
+            m = re.match(r"direct_(\d+)x(\d+)x(\d+)_(v\d+|tp)$", r["config"])
             if r["variant"] == "forced" and m:
-                tr, tc, ch, vi = (int(v) for v in m.groups())
-                cells[(tr, tc), (ch, vi)] = r["tflops"]
+                tr, tc, ch = (int(v) for v in m.groups()[:3])
+                cells[(tr, tc), (ch, m.group(4))] = r["tflops"]
             else:
                 other.append("  %s %s: %.4f ms, %.2f TFLOP/s" % (r["variant"], r["config"], r["ms"], r["tflops"]))
         cols = sorted({c for _, c in cells})
         tiles = sorted({t for t, _ in cells})
         out.append(layer)
-        out.append("  %-10s" % "tile" + "".join("  ch%-3d v%d" % c for c in cols))
+        out.append("  %-10s" % "tile" + "".join("  ch%-3d %-2s" % c for c in cols))
         for t in tiles:
             out.append("  %-10s" % ("%dx%d" % t) +
                        "".join(("%9.1f" % cells[t, c]) if (t, c) in cells else "%9s" % "-" for c in cols))

@@ -171,7 +171,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 25088, 512, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_1 b32 28x28x256->512 3x3 s1
     {1, 0, 0, 25088, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_2 b32 28x28x512->512 3x3 s1
     {1, 0, 0, 6272, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv5_1 b32 14x14x512->512 3x3 s1
-    {1, 0, 0, 401408, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b32 230x230x3->64 7x7 s2
+    {1, 0, 0, 401408, 64, 147, 7, 2, "direct_4x32x64_tp", 1},  // resnet50 conv1_1 b32 230x230x3->64 7x7 s2
     {2, 0, 0, 100352, 256, 64, 1, 1, "gemm_32x256x64_w1x8_nn_v44_o2_br", 1},  // resnet50 conv2_1 b32 56x56x64->256 1x1 s1
     // (kept by hand: inside the benchmark step the B-resident and direct-to-LDS
     // forms, faster alone, take 20.0-20.1 us against this one's 19.5)
@@ -199,7 +199,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 1568, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv5_4 b32 7x7x512->512 3x3 s1
     {2, 0, 0, 1568, 2048, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_5 b32 7x7x512->2048 1x1 s1
     {2, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 6},  // resnet50 conv5_6 b32 7x7x2048->512 1x1 s1
-    {1, 0, 0, 50176, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b1 224x224x3->64 3x3 s1
+    {1, 0, 0, 50176, 64, 27, 3, 1, "direct_4x32x64_tp", 1},  // vgg16 conv1_1 b1 224x224x3->64 3x3 s1
     {1, 0, 0, 50176, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44", 1},  // vgg16 conv1_2 b1 224x224x64->64 3x3 s1
     {1, 0, 0, 12544, 128, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv2_1 b1 112x112x64->128 3x3 s1
     {1, 0, 0, 12544, 128, 1152, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv2_2 b1 112x112x128->128 3x3 s1
@@ -208,7 +208,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 784, 512, 2304, 3, 1, "conv_64x64x32_w2x2_k4_v44_dma2", 2},  // vgg16 conv4_1 b1 28x28x256->512 3x3 s1
     {1, 0, 0, 784, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 12},  // vgg16 conv4_2 b1 28x28x512->512 3x3 s1
     {1, 0, 0, 196, 512, 4608, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 8},  // vgg16 conv5_1 b1 14x14x512->512 3x3 s1
-    {1, 0, 0, 200704, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b4 224x224x3->64 3x3 s1
+    {1, 0, 0, 200704, 64, 27, 3, 1, "direct_8x32x64_tp", 1},  // vgg16 conv1_1 b4 224x224x3->64 3x3 s1
     {1, 0, 0, 200704, 64, 576, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 1},  // vgg16 conv1_2 b4 224x224x64->64 3x3 s1
     {1, 0, 0, 50176, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // vgg16 conv2_1 b4 112x112x64->128 3x3 s1
     {1, 0, 0, 50176, 128, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv2_2 b4 112x112x128->128 3x3 s1
@@ -216,7 +216,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 12544, 256, 2304, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv3_2 b4 56x56x256->256 3x3 s1
     {1, 0, 0, 3136, 512, 2304, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 3},  // vgg16 conv4_1 b4 28x28x256->512 3x3 s1
     {1, 0, 0, 3136, 512, 4608, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2_sk", 1},  // vgg16 conv4_2 b4 28x28x512->512 3x3 s1
-    {1, 0, 0, 12544, 64, 147, 7, 2, "conv_64x64x16_w2x2_v11", 1},  // resnet50 conv1_1 b1 230x230x3->64 7x7 s2
+    {1, 0, 0, 12544, 64, 147, 7, 2, "direct_4x32x32_tp", 1},  // resnet50 conv1_1 b1 230x230x3->64 7x7 s2
     {2, 0, 0, 3136, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b1 56x56x64->256 1x1 s1
     {2, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
     {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 3},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
@@ -242,7 +242,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 49, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv5_4 b1 7x7x512->512 3x3 s1
     {2, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
     {2, 0, 0, 49, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 8},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
-    {1, 0, 0, 50176, 64, 147, 7, 2, "conv_128x64x16_w2x2_v14", 1},  // resnet50 conv1_1 b4 230x230x3->64 7x7 s2
+    {1, 0, 0, 50176, 64, 147, 7, 2, "direct_8x32x32_tp", 1},  // resnet50 conv1_1 b4 230x230x3->64 7x7 s2
     {2, 0, 0, 12544, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b4 56x56x64->256 1x1 s1
     {2, 0, 0, 12544, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b4 56x56x64->64 1x1 s1
     {1, 0, 0, 12544, 64, 576, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 1},  // resnet50 conv2_3 b4 56x56x64->64 3x3 s1
@@ -856,9 +856,14 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
     if (!c) {
         tuned = (KH == KW && sh == sw && find_tuned(conv_kind(gemm_path), 0, 0, M, Cout, K, KH, sh, &tbuf)) ? &tbuf
                                                                                                          : nullptr;
+        // a measured direct configuration (any channel count) needs no workspace
+        const Config *td = tuned ? find_config(tuned->config) : nullptr;
+        if (!gemm_path && td && td->kind == pk::KIND_DIRECT && N <= 65535 &&
+            pk::direct_conv_fits(td, W, Wo, Cout, KH, KW, Cin, sh, sw))
+            return 0;
         const bool direct_ok = !gemm_path && pk::direct_conv_fits(nullptr, W, Wo, Cout, KH, KW, Cin, sh, sw) && N <= 65535;
         if (direct_ok && !(tuned && v4)) return 0;
-        c = (tuned && v4) ? find_config(tuned->config) : nullptr;
+        c = (tuned && v4) ? td : nullptr;
         // a table entry of the other path (never recorded, but checked) is ignored
         if (c && (gemm_path ? !gemm_config_fits(c, 0, 0, v4) : !conv_config_fits(c, true, true))) {
             c = nullptr;
@@ -966,9 +971,10 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     } else {
+        // (the persistent tiled form addresses an image in 32-bit byte offsets)
         auto direct_ok = [&](const Config *d) {
             return N <= 65535 && pk::direct_conv_fits(d, W, Wo, Cout, KH, KW, Cin, sh, sw) &&
-                   (d->vec_a == 1 || va4);
+                   (d->vec_a == 1 || va4) && (d->tile_rows == 0 || !d->persistent || H * W * Cin < ((int64_t)1 << 29));
         };
         // the direct-to-LDS gather addresses the image in 32-bit byte offsets
         const bool dma_ok = (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31);

@@ -396,14 +396,15 @@ TILED_GEOMS = [
 
 def test_tiled_direct_configs_every_instance():
     """Every tiled direct-convolution instance (output tile x channel widths
-    of Section 4.1.1) on windows up to 7x7 stride 2, ragged output tiles and
+    of Section 4.1.1; one tile per work-group, and the persistent form with
+    double-buffered patches, _tp) on windows up to 7x7 stride 2, ragged output tiles and
     channel blocks, odd reductions and asymmetric padding: integer data
     bit-exact against the oracle into a NaN-filled output, and uniform data
     within the bound.  An instance that cannot take a window (LDS, channel
     width) must say so with PK_ERR_NOT_SUPPORTED, never run."""
     torch, pk = require_gpu()
-    tiled = [c for c in pk.configs() if c["kind"] == 2 and c["name"].endswith(("_v1", "_v4"))]
-    assert len(tiled) >= 20
+    tiled = [c for c in pk.configs() if c["kind"] == 2 and c["name"].endswith(("_v1", "_v4", "_tp"))]
+    assert len(tiled) >= 30
     ran = 0
     for gi, (N, H, W, Cin, KH, KW, Cout, stride, pads) in enumerate(TILED_GEOMS):
         rng = np.random.default_rng(500 + gi)
@@ -433,4 +434,4 @@ def test_tiled_direct_configs_every_instance():
                 ran += 1
             finally:
                 pk.force_config(None)
-    assert ran >= 50
+    assert ran >= 70
