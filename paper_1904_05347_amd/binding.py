@@ -19,6 +19,9 @@ PK_ERR_INVALID_VALUE = 1
 PK_ERR_NOT_SUPPORTED = 2
 PK_ERR_WORKSPACE = 3
 PK_ERR_LAUNCH = 4
+PK_ERR_SCRATCH_LIMIT = 5
+# bytes of the static device buffer pk_conv2d_fwd_noalloc works in (PK_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 80 << 20
 
 _lib = None
 _i64 = ctypes.c_int64

@@ -155,6 +155,79 @@ def test_winograd_argument_checks(pk):
     assert call(N=0) == 0
 
 
+def test_noalloc_argument_checks(pk):
+    """pk_conv2d_fwd_noalloc: the argument positions of pk_conv2d_fwd (all
+    checked before the scratch buffer is looked up), and a call whose
+    workspace would exceed the static buffer refused before any work."""
+    from paper_1904_05347_amd import binding
+    fake = 0x10000
+    good = dict(x=fake, N=1, H=5, W=5, Cin=4, f=fake + (1 << 20), KH=3, KW=3, Cout=4, sh=1, sw=1,
+                pt=1, pl=1, pb=1, pr=1, y=fake + (2 << 20), Ho=5, Wo=5)
+    order = list(good)
+    bad = [("N", -1, 2), ("H", 0, 3), ("W", 0, 4), ("Cin", 0, 5), ("KH", 0, 7), ("KW", 0, 8),
+           ("Cout", 0, 9), ("sh", 0, 10), ("sw", 0, 11), ("pt", -1, 12), ("pl", -1, 13),
+           ("pb", -1, 14), ("pr", -1, 15), ("Ho", 4, 17), ("Wo", 6, 18),
+           ("x", None, 1), ("f", None, 6), ("y", None, 16), ("y", fake + 64, 16)]
+    for key, val, pos in bad:
+        args = dict(good)
+        args[key] = val
+        st = binding.conv2d_fwd_noalloc_raw(*[args[k] for k in order])
+        assert (st, pk.last_invalid_param()) == (1, pos), (key, val, st, pk.last_invalid_param())
+    assert binding.conv2d_fwd_noalloc_raw(*[dict(good, N=0)[k] for k in order]) == 0
+    # 1000 output tiles of 128 x 128 over a 576-long reduction: a split of 2,
+    # 2 x 32000 x 512 partial sums (125 MiB), more than the static buffer
+    big = dict(good, H=160, W=200, Cin=64, Cout=512, Ho=160, Wo=200,
+               f=fake + (64 << 20), y=fake + (128 << 20))
+    need = pk.conv2d_workspace_bytes(1, 160, 200, 64, 3, 3, 512, 1, 1, 1, 1, 1, 1)
+    assert need > binding.NOALLOC_SCRATCH_BYTES, need
+    assert binding.conv2d_fwd_noalloc_raw(*[big[k] for k in order]) == binding.PK_ERR_SCRATCH_LIMIT
+    assert "scratch" in binding.load().pk_status_string(binding.PK_ERR_SCRATCH_LIMIT).decode().lower()
+    # the binding's figure is the header's
+    header = open(os.path.join(ROOT, "include", "pk.h")).read()
+    m = re.search(r"#define PK_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", header)
+    assert m and int(m.group(1)) << int(m.group(2)) == binding.NOALLOC_SCRATCH_BYTES
+    m = re.search(r"PK_ERR_SCRATCH_LIMIT = (\d+)", header)
+    assert m and int(m.group(1)) == binding.PK_ERR_SCRATCH_LIMIT
+
+
+def test_winograd_tile_argument_checks(pk):
+    """pk_conv2d_winograd_tile_fwd: the tile size m at position 19 (2 or 4),
+    the workspace at 20, its size from the tile workspace query (36 batched
+    matrices of T = N ceil(Ho/4) ceil(Wo/4) rows for m = 4), and the checks of
+    pk_conv2d_winograd_fwd before them."""
+    from paper_1904_05347_amd import binding
+    fake = 0x10000
+    N, H, W, Cin, Cout = 2, 5, 7, 6, 10
+    need4 = binding.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, 1, 1, 1, 1, tile=4)
+    T4 = N * 2 * 2
+    floor4 = 4 * 36 * (Cin * Cout + T4 * Cin + T4 * Cout)
+    assert floor4 <= need4 < floor4 + 3 * 256, (need4, floor4)
+    assert binding.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, 1, 1, 1, 1, tile=2) == \
+        pk.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, 1, 1, 1, 1)
+    for m in (0, 1, 3, 5, 6):
+        assert binding.conv2d_winograd_workspace_bytes(N, H, W, Cin, Cout, 1, 1, 1, 1, tile=m) == 0
+    ws = fake + (8 << 20)
+    good = dict(x=fake, N=N, H=H, W=W, Cin=Cin, f=fake + (1 << 20), KH=3, KW=3, Cout=Cout, sh=1, sw=1,
+                pt=1, pl=1, pb=1, pr=1, y=fake + (2 << 20), Ho=5, Wo=7, m=4, ws=ws, ws_bytes=need4)
+    order = list(good)
+
+    def call(**kw):
+        args = dict(good, **kw)
+        return binding.conv2d_winograd_tile_raw(*[args[k] for k in order])
+
+    bad = [("N", -1, 2), ("Cin", 0, 5), ("KH", 0, 7), ("pt", -1, 12), ("Ho", 4, 17), ("Wo", 6, 18),
+           ("x", None, 1), ("f", None, 6), ("y", None, 16), ("m", 3, 19), ("m", 0, 19), ("m", 8, 19)]
+    for key, val, pos in bad:
+        st = call(**{key: val})
+        assert (st, pk.last_invalid_param()) == (1, pos), (key, val, st, pk.last_invalid_param())
+    assert call(KH=5, KW=5, pt=2, pl=2, pb=2, pr=2) == 2
+    assert call(sh=2, sw=2, Ho=3, Wo=4) == 2
+    assert call(ws=None) == 3
+    assert call(ws_bytes=need4 - 1) == 3
+    assert (call(ws=ws + 4), pk.last_invalid_param()) == (1, 20)
+    assert call(N=0) == 0
+
+
 def test_direct_to_lds_range_checks(pk):
     """The direct-to-LDS forms address one tile's rows of each operand (and
     a convolution's whole image) in 32-bit byte offsets: a forced one is
