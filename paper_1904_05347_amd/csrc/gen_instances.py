@@ -81,7 +81,8 @@ KSPLIT = [(64, 64, 16, 2, 2, 4, 1, 4, 4, 1), (64, 64, 32, 2, 2, 4, 1, 4, 4, 1), 
 # stages, OCC)
 DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2, 4, 4, 2), (256, 256, 32, 2, 4, 2, 2),
        (128, 128, 32, 2, 4, 2, 2), (128, 128, 32, 2, 4, 3, 2), (128, 128, 32, 2, 4, 4, 2),
-       (128, 128, 16, 2, 2, 3, 1), (128, 128, 16, 2, 2, 4, 1), (64, 64, 32, 2, 2, 3, 1)]
+       (128, 128, 16, 2, 2, 3, 1), (128, 128, 16, 2, 2, 4, 1), (64, 64, 32, 2, 2, 3, 1),
+       (64, 64, 32, 2, 2, 2, 1), (64, 64, 16, 2, 2, 3, 1)]
 
 # K-split forms of the direct-to-LDS contraction ("_kN_..._dmaS"): (BM, BN,
 # BK, WAVES_M, WAVES_N, groups, stages, OCC)
