@@ -164,7 +164,9 @@ const TunedShape kTuned[] = {
     // own choice), one configuration and split per (M, Cout, K, window, stride).
     // Eight 64 x 64 entries later moved to the two-stage (five work-groups per
     // CU) or 64 x 64 x 16 three-stage direct-to-LDS forms, each 3-8 % faster
-    // than the entry it replaced on the same split (graph-timed side by side)
+    // than the entry it replaced on the same split (graph-timed side by side),
+    // and seven more to the search's choice after those forms were added
+    // (3-15 % faster, graph-timed against the entry they replaced)
     {1, 0, 0, 1605632, 64, 27, 3, 1, "direct_8x32x64_k32_p", 1},  // vgg16 conv1_1 b32 224x224x3->64 3x3 s1
     {1, 0, 0, 1605632, 64, 576, 3, 1, "conv_256x64x16_w4x1_v44", 1},  // vgg16 conv1_2 b32 224x224x64->64 3x3 s1
     {1, 0, 0, 401408, 128, 576, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // vgg16 conv2_1 b32 112x112x64->128 3x3 s1
@@ -188,7 +190,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 25088, 128, 1152, 3, 1, "conv_128x128x32_w2x4_v44_o2_dma2", 1},  // resnet50 conv3_4 b32 28x28x128->128 3x3 s1
     {2, 0, 0, 25088, 512, 128, 1, 1, "gemm_64x64x16_w2x2_nn_v44_dma3", 1},  // resnet50 conv3_5 b32 28x28x128->512 1x1 s1
     {2, 0, 0, 25088, 128, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv3_6 b32 28x28x512->128 1x1 s1
-    {1, 0, 0, 6272, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 1},  // resnet50 conv3_7 b32 28x28x128->128 3x3 s2
+    {1, 0, 0, 6272, 128, 1152, 3, 2, "conv_64x64x32_w2x2_k2_v44_dma3", 1},  // resnet50 conv3_7 b32 28x28x128->128 3x3 s2
     {2, 0, 0, 6272, 512, 128, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv4_1 b32 14x14x128->512 1x1 s1
     {2, 0, 0, 6272, 1024, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma2", 1},  // resnet50 conv4_2 b32 14x14x512->1024 1x1 s1
     {2, 0, 0, 6272, 256, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv4_3 b32 14x14x512->256 1x1 s1
@@ -198,7 +200,7 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 1568, 256, 2304, 3, 2, "conv_128x128x32_w2x4_v44_o2_dma2", 9},  // resnet50 conv4_7 b32 14x14x256->256 3x3 s2
     {2, 0, 0, 1568, 1024, 256, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 1},  // resnet50 conv5_1 b32 7x7x256->1024 1x1 s1
     {2, 0, 0, 1568, 2048, 1024, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_2 b32 7x7x1024->2048 1x1 s1
-    {2, 0, 0, 1568, 512, 1024, 1, 1, "gemm_64x64x32_w2x2_k4_nn_v44_d2", 1},  // resnet50 conv5_3 b32 7x7x1024->512 1x1 s1
+    {2, 0, 0, 1568, 512, 1024, 1, 1, "gemm_64x64x32_w2x2_k2_nn_v44_dma3", 1},  // resnet50 conv5_3 b32 7x7x1024->512 1x1 s1
     {1, 0, 0, 1568, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 6},  // resnet50 conv5_4 b32 7x7x512->512 3x3 s1
     {2, 0, 0, 1568, 2048, 512, 1, 1, "gemm_128x128x32_w2x4_nn_v44_o2_dma3", 1},  // resnet50 conv5_5 b32 7x7x512->2048 1x1 s1
     {2, 0, 0, 1568, 512, 2048, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 6},  // resnet50 conv5_6 b32 7x7x2048->512 1x1 s1
@@ -224,7 +226,7 @@ const TunedShape kTuned[] = {
     {2, 0, 0, 3136, 64, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_2 b1 56x56x64->64 1x1 s1
     {1, 0, 0, 3136, 64, 576, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 3},  // resnet50 conv2_3 b1 56x56x64->64 3x3 s1
     {2, 0, 0, 3136, 64, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv2_4 b1 56x56x256->64 1x1 s1
-    {1, 0, 0, 784, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 8},  // resnet50 conv2_5 b1 56x56x64->64 3x3 s2
+    {1, 0, 0, 784, 64, 576, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv2_5 b1 56x56x64->64 3x3 s2
     {2, 0, 0, 784, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv3_1 b1 28x28x64->256 1x1 s1
     {2, 0, 0, 784, 512, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_2 b1 28x28x256->512 1x1 s1
     {2, 0, 0, 784, 128, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv3_3 b1 28x28x256->128 1x1 s1
@@ -234,16 +236,16 @@ const TunedShape kTuned[] = {
     {1, 0, 0, 196, 128, 1152, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv3_7 b1 28x28x128->128 3x3 s2
     {2, 0, 0, 196, 512, 128, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 1},  // resnet50 conv4_1 b1 14x14x128->512 1x1 s1
     {2, 0, 0, 196, 1024, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_2 b1 14x14x512->1024 1x1 s1
-    {2, 0, 0, 196, 256, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
+    {2, 0, 0, 196, 256, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 8},  // resnet50 conv4_3 b1 14x14x512->256 1x1 s1
     {1, 0, 0, 196, 256, 2304, 3, 1, "conv_64x64x32_w2x2_k2_v44_dma3", 12},  // resnet50 conv4_4 b1 14x14x256->256 3x3 s1
     {2, 0, 0, 196, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv4_5 b1 14x14x256->1024 1x1 s1
-    {2, 0, 0, 196, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
+    {2, 0, 0, 196, 256, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_d2", 8},  // resnet50 conv4_6 b1 14x14x1024->256 1x1 s1
     {1, 0, 0, 49, 256, 2304, 3, 2, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv4_7 b1 14x14x256->256 3x3 s2
     {2, 0, 0, 49, 1024, 256, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 1},  // resnet50 conv5_1 b1 7x7x256->1024 1x1 s1
-    {2, 0, 0, 49, 2048, 1024, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 8},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
+    {2, 0, 0, 49, 2048, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 4},  // resnet50 conv5_2 b1 7x7x1024->2048 1x1 s1
     {2, 0, 0, 49, 512, 1024, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 8},  // resnet50 conv5_3 b1 7x7x1024->512 1x1 s1
     {1, 0, 0, 49, 512, 4608, 3, 1, "conv_64x64x32_w2x2_v44_dma3", 16},  // resnet50 conv5_4 b1 7x7x512->512 3x3 s1
-    {2, 0, 0, 49, 2048, 512, 1, 1, "gemm_64x64x32_w2x2_nn_v44_dma3", 12},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
+    {2, 0, 0, 49, 2048, 512, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44", 4},  // resnet50 conv5_5 b1 7x7x512->2048 1x1 s1
     {2, 0, 0, 49, 512, 2048, 1, 1, "gemm_32x64x32_w1x2_k4_nn_v44_dma3", 8},  // resnet50 conv5_6 b1 7x7x2048->512 1x1 s1
     {1, 0, 0, 50176, 64, 147, 7, 2, "direct_8x32x32_tp", 1},  // resnet50 conv1_1 b4 230x230x3->64 7x7 s2
     {2, 0, 0, 12544, 256, 64, 1, 1, "gemm_64x64x64_w2x2_nn_v44_br", 1},  // resnet50 conv2_1 b4 56x56x64->256 1x1 s1
