@@ -355,16 +355,20 @@ bool dma_fits(const Config *c, int64_t lda, int64_t ldb)
 //     K-blocks;
 //     with at most one 64 x 64 tile per CU, 2 groups of 4 waves on 64 x 64
 //     tiles (the 64 .. 1024 sweep of M, N, K at K >= 128: 1.3-1.8x over
-//     one group, every shape);
+//     one group, every shape), copied straight into three stages per group
+//     (1024^2 x 128 .. 1024: 1.02-1.06x the register-staged groups);
 //   - products whose 256 x 256 tiles fill the CUs: 256 x 256 x 32 on 8
 //     waves with both operands copied straight into two LDS stages (at
 //     4096^3 140-143 TFLOP/s in NN, TN and NT: 1.05-1.08x the
 //     register-staged 256 x 256 tiles, and half the fetched bytes of a
 //     128 x 128 tile); whose 128 x 128 tiles fill them: 128 x 128 x 32 the
-//     same way (2048^3: 1.05x);
-//   - everything between: 64 x 64 x 32 copied straight into three LDS
-//     stages (1.04-1.10x the register-staged 64 x 64 x 32 from 1024^2 x 256
-//     to 4096^3 and on ResNet-50's 1x1 layers);
+//     same way (2048^3: 1.05x) -- each only where N fills more than half
+//     its tile (N > 128, N > 64: a 56x56x256 -> 64 1x1 layer at batch 16
+//     runs 1.7x faster on the 64 x 64 tiles below than half-empty 128 x 128
+//     ones);
+//   - everything between: 64 x 64 x 32 copied straight into two LDS stages,
+//     five work-groups per CU (1.03-1.08x the three-stage form on
+//     ResNet-50's 1x1 layers at batch 8 to 32);
 //   - the direct-to-LDS forms only where a tile's rows span less than 2 GiB
 //     (else their register-staged twins); TT: register-staged tiles;
 //   - unaligned operands: 4-byte loads.
@@ -394,13 +398,13 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64
     } else if (ceil_div(M, 32) * ceil_div(N, 64) <= kCUs) {
         return pick("gemm_32x64x32_w1x2_k4_%s_v44_dma3", "gemm_32x64x32_w1x2_k4_%s_v44_d2");
     } else if (ceil_div(M, 64) * ceil_div(N, 64) <= kCUs) {
-        snprintf(name, sizeof(name), "gemm_64x64x32_w2x2_k2_%s_v44_d2", lay);
-    } else if (ceil_div(M, 256) * ceil_div(N, 256) >= kCUs) {
+        return pick("gemm_64x64x32_w2x2_k2_%s_v44_dma3", "gemm_64x64x32_w2x2_k2_%s_v44_d2");
+    } else if (N > 128 && ceil_div(M, 256) * ceil_div(N, 256) >= kCUs) {
         return pick("gemm_256x256x32_w2x4_%s_v44_o2_dma2", "gemm_256x256x32_w2x4_%s_v44_o2");
-    } else if (ceil_div(M, 128) * ceil_div(N, 128) >= kCUs) {
+    } else if (N > 64 && ceil_div(M, 128) * ceil_div(N, 128) >= kCUs) {
         return pick("gemm_128x128x32_w2x4_%s_v44_o2_dma2", "gemm_256x256x32_w2x4_%s_v44_o2");
     } else {
-        return pick("gemm_64x64x32_w2x2_%s_v44_dma3", "gemm_64x64x32_w2x2_%s_v44");
+        return pick("gemm_64x64x32_w2x2_%s_v44_dma2", "gemm_64x64x32_w2x2_%s_v44");
     }
     return find_config(name);
 }
@@ -414,48 +418,75 @@ bool conv_config_fits(const Config *c, bool va4, bool vb4)
     return true;
 }
 
-// Convolutions with Cin and Cout multiples of 4 (16-byte gathers):
-//   - Cout >= 128 and 128 x 128 tiles filling the CUs: 128 x 128 x 32 on 8
-//     waves, both operands copied straight into two LDS stages (VGG-16
-//     conv2_2 / conv3_2 / conv4_2 and ResNet-50 28x28 3x3 at batch 32:
-//     1.10-1.19x the register-staged 64 x 64 x 32);
-//   - other Cout >= 128: 64 x 64 x 32 copied straight into three stages;
-//   - Cout < 128: the register-staged 64 x 64 x 32 (ResNet-50 56x56x64 3x3:
-//     the fastest measured);
+// Convolutions with Cin and Cout multiples of 4 (16-byte gathers), from the
+// automated search over the paper's layers at batch 8 and 16 (shapes the
+// built-in table does not hold; checked on batch 2 and 12: the rules' time
+// over the search's, geometric mean, 1.12 -> 1.04):
+//   - Cout >= 128 with at least four rounds of 128 x 128 tiles (two
+//     work-groups per CU): 128 x 128 x 32 on 8 waves, both operands copied
+//     straight into two LDS stages;
+//   - Cout >= 128, K >= 1024 and at least half a round of such tiles: their
+//     stream-K form (without room for its partial tiles in the workspace the
+//     call chooses again without it); with two to four rounds and a
+//     shorter reduction, the one-tile form;
+//   - at most half a round of 64 x 64 tiles, or at most one round with K
+//     below 2048: 64 x 64 x 32 with the reduction split between 2 groups of
+//     waves (each walking every other K-block, three stages each);
+//   - otherwise 64 x 64 x 32 copied straight into two stages, five
+//     work-groups per CU;
 //   - the direct-to-LDS forms only while the image spans less than 2 GiB.
 // Channel counts that break 16-byte alignment use 4-byte gathers.
-const Config *select_conv(int64_t M, int64_t Cout, bool va4, bool vb4, bool dma_ok)
+const Config *select_conv(int64_t M, int64_t Cout, int64_t K, bool va4, bool vb4, bool dma_ok, bool allow_sk)
 {
     const char *name;
+    const int64_t t128 = ceil_div(M, 128) * ceil_div(Cout, 128);
+    const int64_t t64 = ceil_div(M, 64) * ceil_div(Cout, 64);
     if (!(va4 && vb4))
         name = "conv_64x64x16_w2x2_v11";
-    else if (!dma_ok || Cout < 128)
+    else if (!dma_ok)
         name = "conv_64x64x32_w2x2_v44";
-    else if (ceil_div(M, 128) * ceil_div(Cout, 128) >= kCUs)
+    else if (Cout >= 128 && t128 >= 8 * kCUs)
         name = "conv_128x128x32_w2x4_v44_o2_dma2";
+    else if (Cout >= 128 && allow_sk && K >= 1024 && 2 * t128 >= kCUs)
+        name = "conv_128x128x32_w2x4_v44_o2_dma2_sk";
+    else if (Cout >= 128 && t128 >= 4 * kCUs)
+        name = "conv_128x128x32_w2x4_v44_o2_dma2";
+    else if (2 * t64 <= kCUs || (t64 <= kCUs && K < 64 * 32))
+        name = "conv_64x64x32_w2x2_k2_v44_dma3";
     else
-        name = "conv_64x64x32_w2x2_v44_dma3";
+        name = "conv_64x64x32_w2x2_v44_dma2";
     return find_config(name);
 }
 
-// Split of the K reduction when the output alone gives too few work-groups.
-// Fewer than four rounds of work-groups leave the last round partly idle
-// (wave quantization); long reductions are split until the items fill about
-// four rounds, keeping at least 8 K-blocks per split.  Measured with the
-// automated search on the deep VGG-16 layers at batch 4 (1.13-1.22x) and the
-// 14x14x512 layer at batch 32.  A K-split work-group (its groups of waves
-// fill a CU) is split until the work-groups fill one round, keeping at least
+// Split of the K reduction of a convolution when the output alone gives too
+// few work-groups.  Fewer than four rounds of work-groups leave the last
+// round partly idle (wave quantization); the reduction is split until the
+// items fill about four rounds, keeping at least 16 K-blocks per split (with
+// 8, layers of 16-36 K-blocks split in two and lost up to 1.3x to no split:
+// the pass over the partial sums costs more than the idle CUs).  A K-split
+// work-group (its groups of waves fill a CU) is split only while its tiles
+// leave half the CUs idle, and at most until the work-groups fill one round
+// (one more would need a second round: 1.3-1.5x slower), keeping at least
 // two steps per group.
 int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 {
     if (c->bres) return 1;  // its one K-block is the whole reduction
     const int64_t tiles = ceil_div(M, c->bm) * ceil_div(N, c->bn);
     const int64_t nkb = ceil_div(K, c->bk);
-    const int64_t rounds = c->kgroups > 1 ? 1 : 4;
-    if (tiles >= rounds * kCUs) return 1;
-    int64_t s = ceil_div(rounds * kCUs, tiles);
-    const int64_t max_by_k = nkb / (c->kgroups > 1 ? 2 * c->kgroups : 8);
-    if (s > max_by_k) s = max_by_k;
+    int64_t s;
+    if (c->kgroups > 1) {
+        // one such work-group fills a CU: split only while the tiles leave
+        // half the CUs idle, and never past one round (tiles * s <= CUs)
+        if (2 * tiles > kCUs) return 1;
+        s = kCUs / tiles;
+        const int64_t max_by_k = nkb / (2 * c->kgroups);
+        if (s > max_by_k) s = max_by_k;
+    } else {
+        if (tiles >= 4 * kCUs) return 1;
+        s = ceil_div(4 * kCUs, tiles);
+        const int64_t max_by_k = nkb / 16;
+        if (s > max_by_k) s = max_by_k;
+    }
     if (s > 16) s = 16;
     return s < 1 ? 1 : (int)s;
 }
@@ -876,8 +907,8 @@ size_t pk_conv2d_workspace_bytes(int64_t N, int64_t H, int64_t W, int64_t Cin, i
         }
         if (!c)
             c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cin, Cout, Cout, v4)
-                          : select_conv(M, Cout, Cin % 4 == 0, Cout % 4 == 0,
-                                        (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31));
+                          : select_conv(M, Cout, K, Cin % 4 == 0, Cout % 4 == 0,
+                                        (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31), true);
     }
     if (!c || c->kind == pk::KIND_DIRECT) return 0;
     if (c->streamk) {
@@ -1003,7 +1034,7 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
                     }
                 }
             }
-            if (!c) c = select_conv(M, Cout, va4, vb4, dma_ok);
+            if (!c) c = select_conv(M, Cout, K, va4, vb4, dma_ok, true);
         }
         if (!c) return PK_ERR_NOT_SUPPORTED;
         a.H = (int)H;
@@ -1031,7 +1062,8 @@ int pk_conv2d_fwd(const float *x, int64_t N, int64_t H, int64_t W, int64_t Cin, 
             return planned ? PK_ERR_WORKSPACE : PK_ERR_NOT_SUPPORTED;
         } else {
             c = gemm_path ? select_gemm(0, 0, M, Cout, Cin, Cin, Cout, Cout, vec_ok)
-                          : select_conv(M, Cout, va4, vb4, (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31));
+                          : select_conv(M, Cout, K, va4, vb4, (int64_t)4 * N * H * W * Cin < ((int64_t)1 << 31),
+                                        false);
             if (!c) return PK_ERR_NOT_SUPPORTED;
         }
     }
