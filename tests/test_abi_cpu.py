@@ -174,13 +174,18 @@ def test_noalloc_argument_checks(pk):
         st = binding.conv2d_fwd_noalloc_raw(*[args[k] for k in order])
         assert (st, pk.last_invalid_param()) == (1, pos), (key, val, st, pk.last_invalid_param())
     assert binding.conv2d_fwd_noalloc_raw(*[dict(good, N=0)[k] for k in order]) == 0
-    # 1000 output tiles of 128 x 128 over a 576-long reduction: a split of 2,
-    # 2 x 32000 x 512 partial sums (125 MiB), more than the static buffer
+    # a forced split of 2 over 32000 x 512 outputs: 2 x 32000 x 512 partial
+    # sums (125 MiB), more than the static buffer (the default choices of
+    # this library stay below it: its largest, a stream-K plan, is 64 MiB)
     big = dict(good, H=160, W=200, Cin=64, Cout=512, Ho=160, Wo=200,
                f=fake + (64 << 20), y=fake + (128 << 20))
-    need = pk.conv2d_workspace_bytes(1, 160, 200, 64, 3, 3, 512, 1, 1, 1, 1, 1, 1)
-    assert need > binding.NOALLOC_SCRATCH_BYTES, need
-    assert binding.conv2d_fwd_noalloc_raw(*[big[k] for k in order]) == binding.PK_ERR_SCRATCH_LIMIT
+    pk.force_splits(2)
+    try:
+        need = pk.conv2d_workspace_bytes(1, 160, 200, 64, 3, 3, 512, 1, 1, 1, 1, 1, 1)
+        assert need > binding.NOALLOC_SCRATCH_BYTES, need
+        assert binding.conv2d_fwd_noalloc_raw(*[big[k] for k in order]) == binding.PK_ERR_SCRATCH_LIMIT
+    finally:
+        pk.force_splits(0)
     assert "scratch" in binding.load().pk_status_string(binding.PK_ERR_SCRATCH_LIMIT).decode().lower()
     # the binding's figure is the header's
     header = open(os.path.join(ROOT, "include", "pk.h")).read()
