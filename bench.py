@@ -45,7 +45,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (0 skips it)")
     ap.add_argument("--suite", default="step", choices=("step", "layers", "gemm-sweep", "winograd", "ablations",
-                                                      "tune", "direct"),
+                                                      "tune", "direct", "selector"),
                     help="step: the benchmark step (default); layers: every VGG-16 / ResNet-50 layer of the "
                          "paper at batch 1, 4 and 32; gemm-sweep: the paper's power-of-two GEMM sweep with "
                          "the vendor fp32 GEMM beside it; winograd: the 3x3 stride-1 layers through the "
@@ -53,7 +53,9 @@ def parse():
                          "vector width, wave-tile shape, tile size vs CU fill, operand loader, the convolution's "
                          "gather vs a dense operand, warm vs cold caches; tune: "
                          "the automated parameter search against the built-in choices; direct: every tiled "
-                         "direct-convolution instance (tile x channel widths) on the small-channel layers")
+                         "direct-convolution instance (tile x channel widths) on the small-channel layers; "
+                         "selector: the rules' choice against the automated search on the paper's layers at "
+                         "batch sizes the built-in table does not hold (2, 8, 12, 16)")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the step: measure the fp32 MFMA rate (constant and random operands), "
                          "the HBM copy bandwidth and the vendor fp32 GEMM at 4096^3, print one JSON line")
@@ -824,6 +826,44 @@ def run_tune_suite(torch, pk, wl):
     return {"suite": "tune", "dtype": "f32", "data": "synthetic", "rows": rows}
 
 
+def run_selector_suite(torch, pk, wl, batches=(2, 8, 12, 16)):
+    """How the selection rules generalise: every layer of the paper's tables
+    (square windows and strides) at batch sizes the built-in table does not
+    hold, timed with the rules' choice, then with the automated search's
+    choice (pk_tune_conv2d_fwd on the same operands, splits up to 16), both
+    by graph replay; the ratio of the two times is what the rules leave on
+    the table for shapes nobody measured."""
+    rows = []
+    for batch in batches:
+        for case in wl.layer_suite(batch):
+            N, H, W, Cin = case.x_shape
+            KH, KW, _, Cout = case.f_shape
+            if KH != KW or case.stride[0] != case.stride[1]:
+                continue
+            x, f = case.inputs()
+            Ho, Wo = pk.conv2d_out_dims(H, W, KH, KW, *case.stride, *case.pads)
+            dx, df = torch.from_numpy(x).cuda(), torch.from_numpy(f).cuda()
+            dy = torch.empty((N, Ho, Wo, Cout), dtype=torch.float32, device="cuda")
+            wsb = pk.conv2d_workspace_bytes(N, H, W, Cin, KH, KW, Cout, *case.stride, *case.pads)
+            ws = torch.empty(max(wsb // 4, 1), dtype=torch.float32, device="cuda")
+            pk.tune_reset()
+            ms_r = _time_ms_graph(torch, lambda: pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads,
+                                                              out=dy, workspace=ws))
+            cfg_r = pk.last_config_name()
+            wst = torch.empty(min(16 * N * Ho * Wo * Cout, 1 << 29), dtype=torch.float32, device="cuda")
+            r = pk.tune_conv2d(dx, df, stride=case.stride, padding=case.pads, out=dy, workspace=wst, iters=3)
+            ms_s = _time_ms_graph(torch, lambda: pk.conv2d_fwd(dx, df, stride=case.stride, padding=case.pads,
+                                                              out=dy, workspace=wst))
+            pk.tune_reset()
+            rows.append({"layer": case.name, "rules": cfg_r, "ms_rules": round(ms_r, 4), "search": r["config"],
+                         "search_splits": r["splits"], "ms_search": round(ms_s, 4),
+                         "rules_over_search": round(ms_r / ms_s, 3)})
+            print("bench: %s rules %s %.4f ms, search %s/%d %.4f ms" % (case.name, cfg_r, ms_r, r["config"],
+                  r["splits"], ms_s), file=sys.stderr, flush=True)
+            del dx, df, dy, ws, wst
+    return {"suite": "selector", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
 def run_gemm_sweep(torch, pk, wl):
     """The paper's GEMM sweep (M, N, K powers of two in [64, 1024]), with the
     vendor fp32 GEMM (torch.matmul, tf32 off) timed beside it as context."""
@@ -908,6 +948,9 @@ def main():
     if args.suite == "direct":
         res = run_direct_suite(torch, pk, wl)
         print(direct_heatmap(res) if args.text else json.dumps(res))
+        return
+    if args.suite == "selector":
+        print(json.dumps(run_selector_suite(torch, pk, wl)))
         return
     if args.suite == "tune":
         print(json.dumps(run_tune_suite(torch, pk, wl)))
