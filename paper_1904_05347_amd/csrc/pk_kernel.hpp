@@ -383,13 +383,26 @@ struct GemmTile {
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     }
 
+    // Row of C that acc[i][*][r] of a lane holds.  The MFMA puts row slot
+    // 8*(r/4) + r%4 + 4h of block i's A operand in register r of lane
+    // (l32, h).  Blocked rows (ILV false): block i is rows 32i .. 32i+31 of
+    // the wave tile, row_base = the wave's first row + 4h.  Interleaved rows
+    // (ILV true): slot s of block i is row RM*s + i, so a lane's RM blocks
+    // read RM adjacent rows (one 16-byte LDS read for RM = 4 where A is
+    // m-contiguous), row_base = the wave's first row + RM*4h.
+    template <bool ILV>
+    static __device__ __forceinline__ int row_of(int row_base, int i, int r)
+    {
+        return ILV ? row_base + RM * (8 * (r >> 2) + (r & 3)) + i : row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+    }
+
     // Epilogue of one tile: C = alpha * acc (+ beta * C when BETA), or split
     // z's partial sum alpha * acc into the workspace.  Lane (l32, h) of the
-    // wave holds C(row_base + i*32 + 8*(r/4) + r%4, col_base + j*32) in
+    // wave holds C(row_of<ILV>(row_base, i, r), col_base + j*32) in
     // acc[i][j][r].  BETA = false never reads C (beta == 0).  C is written
     // with non-temporal stores (this launch does not read it again): 2-4 %
     // faster on the HBM-bound ResNet-50 1x1 layers, no change on the others.
-    template <bool BETA>
+    template <bool BETA, bool ILV = false>
     static __device__ __forceinline__ void store(const KernelArgs &p, const Acc &acc, int row_base, int col_base,
                                                  int z)
     {
@@ -399,7 +412,7 @@ struct GemmTile {
             for (int i = 0; i < RM; ++i)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                    const int row = row_of<ILV>(row_base, i, r);
                     if (row < p.M) {
 #pragma unroll
                         for (int j = 0; j < RN; ++j) {
@@ -415,7 +428,7 @@ struct GemmTile {
             for (int i = 0; i < RM; ++i)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                    const int row = row_of<ILV>(row_base, i, r);
                     if (row < p.M) {
                         float *crow = p.C + (int64_t)row * p.ldc;
 #pragma unroll
@@ -432,14 +445,14 @@ struct GemmTile {
             // computed next to its own store makes every store wait for the
             // one before it (a load that follows a store to C cannot be moved
             // above it by the compiler).  Interior lanes skip the bounds tests.
-            const bool interior = row_base + (RM - 1) * 32 + 27 < p.M && col_base + (RN - 1) * 32 < p.N;
+            const bool interior = row_of<ILV>(row_base, RM - 1, 15) < p.M && col_base + (RN - 1) * 32 < p.N;
             const float alpha = p.alpha, beta = p.beta;
 #pragma unroll
             for (int i = 0; i < RM; ++i) {
                 float v[16][RN];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                    const int row = row_of<ILV>(row_base, i, r);
                     const float *crow = p.C + (int64_t)row * p.ldc;
 #pragma unroll
                     for (int j = 0; j < RN; ++j) {
@@ -456,7 +469,7 @@ struct GemmTile {
                     }
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int row = row_base + i * 32 + 8 * (r >> 2) + (r & 3);
+                    const int row = row_of<ILV>(row_base, i, r);
                     float *crow = p.C + (int64_t)row * p.ldc;
 #pragma unroll
                     for (int j = 0; j < RN; ++j) {
@@ -666,6 +679,21 @@ struct DmaOperand {
             for (int t = 0; t < 4; ++t) v[t] = tile[(k + t) * R + col];
         }
     }
+    // m-contiguous layout: the same four k of the four adjacent rows row ..
+    // row+3 (row a multiple of 4, so they are one 16-byte chunk, which the
+    // swizzle moves whole), one 16-byte read per k: v[i][t] is row row+i
+    template <typename Frag>
+    __device__ __forceinline__ static void read4_rows4(const float *tile, int row, int h, int g, Frag &v)
+    {
+        static_assert(!KROWS, "adjacent rows share a chunk only in the m-contiguous layout");
+        const int k = h * (BK / 2) + 4 * g;
+        const int col = row ^ (32 * h);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const f32x4 x = *reinterpret_cast<const f32x4 *>(tile + (k + t) * R + col);
+            v[0][t] = x[0]; v[1][t] = x[1]; v[2][t] = x[2]; v[3][t] = x[3];
+        }
+    }
 };
 
 // The implicit-GEMM gather of A (NHWC image, Cin % 4 == 0) copied straight
@@ -820,11 +848,19 @@ gemm_dma_kernel(KernelArgs p)
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
     };
-    const int a_row = wm * G::WM + l32;
+    // an m-contiguous A tile with four 32-row blocks per wave takes them
+    // interleaved (GemmTile::row_of): one 16-byte LDS read per k for all four
+    // blocks instead of a read of two k per block
+    constexpr bool ILV = AMODE == A_MCONTIG && G::RM == 4;
+    const int a_row = wm * G::WM + (ILV ? 4 * l32 : l32);
     const int b_row = wn * G::WN + l32;
     auto read_group = [&](const float *as, int g, typename G::FragA &xa, typename G::FragB &xb) {
+        if constexpr (ILV) {
+            OpA::read4_rows4(as, a_row, h, g, xa);
+        } else {
 #pragma unroll
-        for (int i = 0; i < G::RM; ++i) OpA::read4(as, a_row + i * 32, h, g, xa[i]);
+            for (int i = 0; i < G::RM; ++i) OpA::read4(as, a_row + i * 32, h, g, xa[i]);
+        }
 #pragma unroll
         for (int j = 0; j < G::RN; ++j) OpB::read4(as + A_ST, b_row + j * 32, h, g, xb[j]);
     };
@@ -892,7 +928,7 @@ gemm_dma_kernel(KernelArgs p)
         s = s_next;
     }
 
-    G::template store<BETA>(p, acc, m0 + wm * G::WM + 4 * h, n0 + wn * G::WN + l32, blockIdx.z);
+    G::template store<BETA, ILV>(p, acc, m0 + wm * G::WM + (ILV ? 16 * h : 4 * h), n0 + b_row, blockIdx.z);
 }
 
 // The same contraction with the global loads TWO K-blocks ahead: two
