@@ -87,7 +87,7 @@ DMA = [(256, 256, 16, 2, 4, 2, 2), (256, 256, 16, 2, 4, 3, 2), (256, 256, 16, 2,
 # K-split forms of the direct-to-LDS contraction ("_kN_..._dmaS"): (BM, BN,
 # BK, WAVES_M, WAVES_N, groups, stages, OCC)
 DMA_KSPLIT = [(32, 64, 32, 1, 2, 4, 2, 1), (32, 64, 32, 1, 2, 4, 3, 1), (64, 64, 32, 2, 2, 2, 2, 1),
-              (64, 64, 32, 2, 2, 2, 3, 1), (32, 64, 16, 1, 2, 8, 3, 1)]
+              (64, 64, 32, 2, 2, 2, 3, 1), (32, 64, 16, 1, 2, 8, 3, 1), (64, 64, 32, 2, 2, 4, 2, 1)]
 
 # ... and for the convolution's gather: few output tiles, long reductions
 # (deep layers at small batch, strided 1x1 layers).
