@@ -400,6 +400,7 @@ const Config *select_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, int64
     } else if (ceil_div(M, 32) * ceil_div(N, 64) <= kCUs) {
         return pick("gemm_32x64x32_w1x2_k4_%s_v44_dma3", "gemm_32x64x32_w1x2_k4_%s_v44_d2");
     } else if (ceil_div(M, 64) * ceil_div(N, 64) <= kCUs) {
+        if (K >= 1024) return pick("gemm_64x64x32_w2x2_k4_%s_v44_dma2", "gemm_64x64x32_w2x2_k2_%s_v44_d2");
         return pick("gemm_64x64x32_w2x2_k2_%s_v44_dma3", "gemm_64x64x32_w2x2_k2_%s_v44_d2");
     } else if (N > 128 && ceil_div(M, 256) * ceil_div(N, 256) >= kCUs) {
         return pick("gemm_256x256x32_w2x4_%s_v44_o2_dma2", "gemm_256x256x32_w2x4_%s_v44_o2");
@@ -496,12 +497,15 @@ int choose_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 // A GEMM's split of K: only when the tiles fill less than one round of the
 // CUs (a product that large is bound by its tiles' K loops, not by wave
 // quantization, and every split costs a pass over M x N partial sums), until
-// the work-groups fill about one round (K-split forms: one per CU; others:
-// two), keeping at least 8 K-blocks (K-split forms: one step per group) per
-// split.  A K-split form splits only when each group would walk at least 4
-// steps without it: the reduce kernel's launch (about 2 us in a graph) costs
-// more than 1 step saved (the GEMM sweep: at K = 256 a split of 2 loses up
-// to 1.25x; at K = 512, 4 splits beat none by up to 0.9 us).
+// the work-groups fill about one round (K-split forms, one work-group per
+// CU: never past one round, as for the convolutions -- 200 tiles split in
+// two ran in two rounds plus the reduce, 46 against 41 us unsplit; others:
+// about two per CU), keeping at least 8 K-blocks (K-split forms: one step
+// per group) per split.  A K-split form splits only when each group would
+// walk at least 4 steps without it: the reduce kernel's launch (about 2 us
+// in a graph) costs more than 1 step saved (the GEMM sweep: at K = 256 a
+// split of 2 loses up to 1.25x; at K = 512, 4 splits beat none by up to
+// 0.9 us).
 int gemm_splits(const Config *c, int64_t M, int64_t N, int64_t K)
 {
     if (c->bres) return 1;
@@ -509,7 +513,7 @@ int gemm_splits(const Config *c, int64_t M, int64_t N, int64_t K)
     const int64_t nkb = ceil_div(K, c->bk);
     if (tiles >= kCUs) return 1;
     if (c->kgroups > 1 && nkb < 4 * c->kgroups) return 1;
-    int64_t s = ceil_div((c->kgroups > 1 ? 1 : 2) * kCUs, tiles);
+    int64_t s = c->kgroups > 1 ? kCUs / tiles : ceil_div(2 * kCUs, tiles);
     const int64_t max_by_k = nkb / (c->kgroups > 1 ? c->kgroups : 8);
     if (s > max_by_k) s = max_by_k;
     if (s > 16) s = 16;
