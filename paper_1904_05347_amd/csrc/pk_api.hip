@@ -358,7 +358,10 @@ bool dma_fits(const Config *c, int64_t lda, int64_t ldb)
 //     with at most one 64 x 64 tile per CU, 2 groups of 4 waves on 64 x 64
 //     tiles (the 64 .. 1024 sweep of M, N, K at K >= 128: 1.3-1.8x over
 //     one group, every shape), copied straight into three stages per group
-//     (1024^2 x 128 .. 1024: 1.02-1.06x the register-staged groups);
+//     (1024^2 x 128 .. 1024: 1.02-1.06x the register-staged groups); from
+//     K = 1024 on, 4 groups of 4 waves with two stages each (1024^3 and
+//     three ResNet-50 1x1 layers with K = 1024 at batch 8 to 16:
+//     1.02-1.03x; at K = 128 .. 512 they lose 3-15 %);
 //   - products whose 256 x 256 tiles fill the CUs: 256 x 256 x 32 on 8
 //     waves with both operands copied straight into two LDS stages (at
 //     4096^3 140-143 TFLOP/s in NN, TN and NT: 1.05-1.08x the
