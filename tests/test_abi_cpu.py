@@ -306,6 +306,11 @@ def test_gemm_workspace_checks(pk):
     assert binding.sgemm_workspace_bytes("N", "N", 64, 64, 64) == 0
     need = binding.sgemm_workspace_bytes("N", "N", 64, 64, 1024)
     assert need > 0 and need % per_split == 0
+    # a K-split form (one work-group per CU) never splits past one round of
+    # work-groups (256 CUs): 200 tiles of 64 x 64 with K = 2048 take no
+    # split, 80 tiles of 32 x 64 a split of 3 (rounding up would take 4)
+    assert binding.sgemm_workspace_bytes("N", "N", 1600, 512, 2048) == 0
+    assert binding.sgemm_workspace_bytes("N", "N", 320, 512, 2048) == 3 * 320 * 512 * 4
 
 
 def test_tune_argument_checks(pk):
