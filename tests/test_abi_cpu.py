@@ -372,6 +372,39 @@ def test_config_space(pk):
             assert {1, 4} <= vecs
 
 
+def test_selection_names_exist(pk):
+    """Every configuration the built-in table or the selection rules name is
+    compiled (a misspelt name would silently fall back to the rules): the
+    table entries, the convolution rules, and the GEMM rules' name patterns
+    for each layout they serve (tiled and direct-to-LDS forms for NN, TN and
+    NT, the B-resident form for NN, the scalar-load and TT forms for TT)."""
+    names = {c["name"] for c in pk.configs()}
+    src = open(os.path.join(ROOT, "paper_1904_05347_amd", "csrc", "pk_api.hip")).read()
+    a = src.index("const TunedShape kTuned[] = {")
+    table = re.findall(r'"((?:gemm|conv|direct)_[a-z0-9_]+)"', src[a:src.index("};", a)])
+    assert len(table) >= 100
+    assert set(table) <= names, sorted(set(table) - names)
+    conv = src[src.index("const Config *select_conv"):]
+    conv = re.findall(r'"(conv_[a-z0-9_]+)"', conv[:conv.index("\n}\n")])
+    assert len(conv) >= 5 and set(conv) <= names, sorted(set(conv) - names)
+    body = src[src.index("const Config *select_gemm"):]
+    body = body[:body.index("\n}\n")]
+    # pick(direct-to-LDS form, register-staged twin): the first for NN, and
+    # for every layout one of the two (32-row tiles have no TN copy form)
+    pairs = re.findall(r'pick\("(gemm_[a-z0-9_%]+)", "(gemm_[a-z0-9_%]+)"\)', body)
+    assert len(pairs) >= 5
+    for dma, reg in pairs:
+        assert dma % "nn" in names, dma % "nn"
+        for lay in ("nn", "tn", "nt"):
+            assert dma % lay in names or reg % lay in names, (dma % lay, reg % lay)
+    single = set(re.findall(r'"(gemm_[a-z0-9_]+%s[a-z0-9_]*)"', body)) - {n for pr in pairs for n in pr}
+    assert len(single) >= 4
+    for pat in single:
+        layouts = ["nn"] if pat.endswith("_br") else ["nn", "tn", "nt", "tt"]
+        for lay in layouts:
+            assert pat % lay in names, pat % lay
+
+
 def test_force_config_and_status_strings(pk):
     from paper_1904_05347_amd import binding
     with pytest.raises(pk.PkError):
