@@ -293,15 +293,17 @@ def test_persistent_conv_configs_loop_over_tiles(splits):
         assert np.array_equal(out.reshape(-1)[idx].astype(np.float64), ref), cfg["name"]
 
 
-SUITE = [(b, c) for b in (1, 4, 32) for c in wl.layer_suite(b)]
+# batch 1, 4 and 32 (the built-in table's shapes) and 2 and 12 (shapes the
+# table does not hold: the selection rules' own configurations and splits)
+SUITE = [(b, c) for b in (1, 2, 4, 12, 32) for c in wl.layer_suite(b)]
 
 
 @pytest.mark.parametrize("batch,case", SUITE, ids=[c.name for _, c in SUITE])
 def test_paper_layer_suite(batch, case):
-    """Every distinct VGG-16 / ResNet-50 layer of the paper at batch 1, 4, 32,
-    into a NaN-filled output: the whole output where the oracle is quick,
-    else the corners of every output tile and sampled outputs (every border
-    class included)."""
+    """Every distinct VGG-16 / ResNet-50 layer of the paper at batch 1, 2, 4,
+    12 and 32, into a NaN-filled output: the whole output where the oracle is
+    quick, else the corners of every output tile and sampled outputs (every
+    border class included)."""
     from tests.test_gpu_fullsize import _conv_tile_corners
     torch, pk = require_gpu()
     x, f = case.inputs()
