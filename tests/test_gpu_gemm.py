@@ -281,6 +281,45 @@ def test_ksplit_configs():
     assert ran >= 36
 
 
+# One shape per branch of the GEMM selection rules, none of them in the
+# built-in table, with the configuration each branch picks (the workspace the
+# library asks for, so the rules' splits run too).
+RULE_SHAPES = [
+    ("N", "N", 100, 70, 33, "gemm_64x64x16_w2x2_nn_v11"),              # unaligned: 4-byte loads
+    ("T", "T", 300, 260, 96, "gemm_64x64x16_w2x2_tt_v44"),             # TT, few tiles
+    ("N", "N", 1000, 128, 64, "gemm_64x64x64_w2x2_nn_v44_br"),         # K = 64: B resident
+    ("T", "N", 1000, 128, 64, "gemm_64x64x16_w2x2_tn_v44"),
+    ("N", "N", 320, 512, 2048, "gemm_32x64x32_w1x2_k4_nn_v44_dma3"),   # 80 tiles: K split 4 ways inside, 3 across
+    ("T", "N", 320, 512, 2048, "gemm_32x64x32_w1x2_k4_tn_v44_d2"),     # (no TN copy form for 32 rows)
+    ("N", "T", 320, 512, 2048, "gemm_32x64x32_w1x2_k4_nt_v44_dma3"),
+    ("N", "N", 1600, 512, 1024, "gemm_64x64x32_w2x2_k4_nn_v44_dma2"),  # 200 tiles, K >= 1024: four groups
+    ("T", "N", 1600, 512, 1024, "gemm_64x64x32_w2x2_k4_tn_v44_dma2"),
+    ("N", "T", 1600, 512, 1024, "gemm_64x64x32_w2x2_k4_nt_v44_dma2"),
+    ("N", "N", 1600, 512, 512, "gemm_64x64x32_w2x2_k2_nn_v44_dma3"),   # shorter K: two groups
+    ("N", "N", 2048, 2048, 128, "gemm_128x128x32_w2x4_nn_v44_o2_dma2"),  # 128 x 128 tiles fill the CUs
+    ("N", "N", 20000, 64, 256, "gemm_64x64x32_w2x2_nn_v44_dma2"),      # everything between
+    ("T", "N", 20000, 64, 256, "gemm_64x64x32_w2x2_tn_v44_dma2"),
+]
+
+
+@pytest.mark.parametrize("ta,tb,M,N,K,want", RULE_SHAPES,
+                         ids=["%s%s_%dx%dx%d" % r[:5] for r in RULE_SHAPES])
+def test_gemm_rule_branches(ta, tb, M, N, K, want):
+    """Each branch of the selection rules on a shape outside the table: the
+    configuration it picks, with its split, equals the oracle bit for bit
+    on integer data (beta = 0.5)."""
+    torch, pk = require_gpu()
+    rng = np.random.default_rng(M + 3 * N + 7 * K)
+    A = wl.integers(rng, M * K).reshape((K, M) if ta == "T" else (M, K))
+    B = wl.integers(rng, K * N).reshape((N, K) if tb == "T" else (K, N))
+    C = wl.integers(rng, M * N).reshape(M, N)
+    dC = dev(C)
+    pk.gemm(dev(A), dev(B), dC, alpha=1.0, beta=0.5, trans_a=ta == "T", trans_b=tb == "T")
+    assert pk.last_config_name() == want
+    ref, _ = oracle.sgemm(ta, tb, M, N, K, 1.0, A, A.shape[1], B, B.shape[1], 0.5, C, N)
+    assert np.array_equal(host(dC).astype(np.float64), ref), (ta, tb, M, N, K, want)
+
+
 def test_column_major_swap_identity():
     """A column-major C = A B is the row-major call with operands swapped."""
     torch, pk = require_gpu()
